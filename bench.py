@@ -1,0 +1,316 @@
+"""Benchmark: one CURE verify-and-repair step on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM:
+  1. cure_margins   over every tree node's logits row, with the UFP gate over
+                    the draft-chain rows (Sec. 3.3, Eq. 2, Algorithm 1),
+  2. cure_tree_attn one tree-masked verification attention layer (Sec. 3.5),
+  3. cure_accept    the acceptance walk, fed the margins' top-1 indices as the
+                    target argmax (Eq. 1, Eq. 4).
+
+Timing: each input copy's step is captured once as a HIP graph; W warm-up
+replays, then exactly K replays (K steps) bracketed by synchronize() on both
+sides, timed by the host clock (ms_per_step) and by HIP events on the launch
+stream. Inputs rotate over enough copies (>= 512 MB in total) that each step
+reads from HBM rather than the 256 MB last-level cache. A second timed region
+launches the calls eagerly with HIP events around each one (behind a spin
+kernel, so host launch cost stays off the GPU timeline) to give the per-call
+durations used for the roofline.
+
+The printed JSON line's `value` is the step's algorithmic bytes over its time
+(GB/s). `cpu_baseline` times the CPU oracle on a bounded sample of the same
+workload on this host.
+"""
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tree-verify step latency (µs) + KV GB/s vs HBM peak, Llama-3-8B attn shape"
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "llama3_8b_ctx2k_b1"
+ROTATE_BYTES = 512 << 20
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="approximate CPU time spent on the oracle baseline (0 = skip)")
+    p.add_argument("--no-rotate", action="store_true",
+                   help="reuse one input copy (cache-warm numbers; never the headline)")
+    return p.parse_args()
+
+
+class Step:
+    """Pre-bound C-ABI calls for one input copy (argument marshalling done once)."""
+
+    def __init__(self, pc, torch, w, copy, stream):
+        L = pc.lib()
+        self.L = L
+        dev = torch.device("cuda")
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        B, R, V = w.batch, w.n_max, w.vocab
+        self.keep = [copy]
+        self.m = {k: torch.empty(B, R, **(f32 if k in ("top1_val", "top2_val", "lse", "margin") else i32))
+                  for k in ("top1_val", "top1_idx", "top2_val", "top2_idx", "lse", "margin")}
+        self.ufp_pos = torch.empty(B, w.chain_len, **i32)
+        self.ufp_cnt = torch.empty(B, **i32)
+        self.o = torch.empty(B, R, w.hq, w.d, dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty(B, R, w.hq, **f32)
+        self.status = torch.empty(B, **i32)
+        self.acc = {k: torch.empty(B, **i32) for k in ("acc_len", "best", "bonus", "resync")}
+        self.path = torch.empty(B, R, **i32)
+        self.host_ctx = np.ascontiguousarray(w.ctx_len, np.int32)
+        self.host_nn = np.ascontiguousarray(w.n_nodes, np.int32)
+        hc = self.host_ctx.ctypes.data_as(ctypes.c_void_p)
+        hn = self.host_nn.ctypes.data_as(ctypes.c_void_p)
+        mws = L.cure_margins_workspace_size(B, R, V)
+        self.mws = torch.zeros(max(mws, 256), dtype=torch.uint8, device=dev)
+        aws = L.cure_tree_attn_workspace_size(B, w.hq, w.hkv, w.d, R, hc, hn, 0)
+        self.aws = torch.zeros(max(aws, 256), dtype=torch.uint8, device=dev)
+        P = lambda t: ctypes.c_void_p(t.data_ptr())
+        s = ctypes.c_void_p(stream)
+        self.margins_args = (
+            P(copy["logits"]), pc.CURE_BF16 if w.dtype == "bf16" else pc.CURE_F32, B, R, V, V,
+            P(self.m["top1_val"]), P(self.m["top1_idx"]), P(self.m["top2_val"]),
+            P(self.m["top2_idx"]), P(self.m["lse"]), P(self.m["margin"]), w.chain_len,
+            ctypes.c_float(w.tau), w.repair_budget, w.branch_depth, P(self.ufp_pos),
+            P(self.ufp_cnt), P(self.mws), self.mws.numel(), s)
+        self.attn_args = (
+            P(copy["q"]), P(copy["k"]), P(copy["v"]), P(self.o), P(self.lse),
+            pc.CURE_BF16 if w.dtype == "bf16" else pc.CURE_F32, pc.CURE_BF16, B, w.hq, w.hkv,
+            w.d, ctypes.c_float(w.scale), P(copy["kv_off"]), P(copy["ctx_len"]),
+            P(copy["n_nodes"]), P(copy["parent"]), R, hc, hn, 0, 0, P(self.status),
+            P(self.aws), self.aws.numel(), s)
+        self.accept_args = (
+            P(copy["parent"]), P(copy["token"]), P(self.m["top1_idx"]), P(copy["root_tgt"]),
+            P(copy["n_nodes"]), w.chain_len, B, R, P(self.acc["acc_len"]), P(self.path),
+            P(self.acc["best"]), P(self.acc["bonus"]), P(self.acc["resync"]), s)
+
+    def margins(self):
+        st = self.L.cure_margins(*self.margins_args)
+        if st:
+            raise RuntimeError("cure_margins status %d" % st)
+
+    def attn(self):
+        st = self.L.cure_tree_attn(*self.attn_args)
+        if st:
+            raise RuntimeError("cure_tree_attn status %d" % st)
+
+    def accept(self):
+        st = self.L.cure_accept(*self.accept_args)
+        if st:
+            raise RuntimeError("cure_accept status %d" % st)
+
+    def run(self):
+        self.margins()
+        self.attn()
+        self.accept()
+
+
+def upload_copy(torch, w):
+    def dev(a, bf16=False):
+        a = np.ascontiguousarray(a)
+        if bf16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+    bf = w.dtype == "bf16"
+    return {
+        "logits": dev(w.logits, bf), "q": dev(w.q, bf), "k": dev(w.k, bf), "v": dev(w.v, bf),
+        "kv_off": dev(w.kv_off), "ctx_len": dev(w.ctx_len), "n_nodes": dev(w.n_nodes),
+        "parent": dev(w.parent), "token": dev(w.token), "root_tgt": dev(w.root_tgt),
+    }
+
+
+def replicate(torch, base):
+    """A fresh device copy of the large inputs (so each lives at its own address)."""
+    c = dict(base)
+    for k in ("logits", "q", "k", "v"):
+        c[k] = base[k].clone()
+    return c
+
+
+def spin(torch, us):
+    """Queue a spin kernel of about `us` microseconds on the current stream."""
+    torch.cuda._sleep(int(us * 2400))          # cycles at ~2.4 GHz
+
+
+def capture(torch, steps, stream):
+    """One HIP graph per input copy, each holding one whole step."""
+    graphs = []
+    for st in steps:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            st.run()
+        graphs.append(g)
+    return graphs
+
+
+def timed_steps(torch, graphs, k, warmup):
+    """Exactly k graph replays (one step each), bracketed by synchronize()."""
+    n = len(graphs)
+    for i in range(warmup):
+        graphs[i % n].replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(k):
+        graphs[i % n].replay()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall * 1e3 / k, start.elapsed_time(end) / k
+
+
+def per_call_times(torch, steps, k):
+    """Average GPU duration of each call, from events around every eager launch.
+    A spin kernel queued first keeps the host's launch cost off the GPU timeline."""
+    names = ("margins", "attn", "accept")
+    n = len(steps)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(k)]
+    torch.cuda.synchronize()
+    spin(torch, 20000)
+    for i in range(k):
+        s = steps[i % n]
+        ev[i][0].record()
+        s.margins()
+        ev[i][1].record()
+        s.attn()
+        ev[i][2].record()
+        s.accept()
+        ev[i][3].record()
+    torch.cuda.synchronize()
+    out = {}
+    for j, name in enumerate(names):
+        out[name] = float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(k)])) * 1e3
+    return out
+
+
+def cpu_baseline(w, algo_bytes, budget_s):
+    import oracle
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = 1
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        for b in range(w.batch):
+            m = oracle.margins(w.logits[b], w.dtype)
+            oracle.ufp_select(m["margin_f32"][: w.chain_len], w.tau, w.repair_budget,
+                              w.branch_depth)
+            oracle.accept(w.parent[b], w.token[b], m["top1_idx"], int(w.root_tgt[b]),
+                          int(w.n_nodes[b]), w.chain_len)
+        oracle.tree_attention(w.q, w.k, w.v, w.dtype, w.kv_off, w.ctx_len, w.n_nodes,
+                              w.parent, w.hq, w.hkv, w.scale)
+        reps += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = (time.perf_counter() - t0) / reps
+    return {"value": round(algo_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle", "ms_per_step": round(dt * 1e3, 1),
+            "sample": "%d full oracle step(s) of workload %s (margins+UFP and accept per "
+                      "sequence, float64 tree attention for every node and head); BLAS "
+                      "threads=%d, sorts single-threaded" % (reps, w.name, threads)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_00531_amd as pc
+    from synth import preset, algorithmic_bytes
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = preset(args.workload)
+    ab = algorithmic_bytes(w)
+    step_bytes = ab["attention"] + ab["margins"] + ab["accept"]
+    base = upload_copy(torch, w)
+    per_copy = sum(base[k].numel() * base[k].element_size() for k in ("logits", "q", "k", "v"))
+    ncopy = 1 if args.no_rotate else max(3, math.ceil(ROTATE_BYTES / per_copy))
+    copies = [base] + [replicate(torch, base) for _ in range(ncopy - 1)]
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        steps = [Step(pc, torch, w, c, stream.cuda_stream) for c in copies]
+        for st in steps:                       # eager reference results, one per copy
+            st.run()
+        torch.cuda.synchronize()
+        ref = [(st.m["top1_idx"].clone(), st.acc["acc_len"].clone(), st.o.clone())
+               for st in steps]
+        graphs = capture(torch, steps, stream)
+        ms, ev_ms = timed_steps(torch, graphs, args.steps, args.warmup)
+        # Every graph's last replay must reproduce the eager results.
+        for st, (t1, al, o) in zip(steps, ref):
+            assert torch.equal(st.m["top1_idx"], t1) and torch.equal(st.acc["acc_len"], al)
+            assert torch.equal(st.o, o)
+        calls = per_call_times(torch, steps, min(args.steps, 100))
+    status = steps[0].status.cpu().tolist()
+    assert status == [0] * w.batch, status
+
+    call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"]}
+    kernels = {}
+    for name, us in calls.items():
+        gbs = call_bytes[name] / (us * 1e-6) / 1e9
+        kernels[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
+                         "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    dom = max(calls, key=calls.get)
+    dom_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
+    names = {"margins": "cure_margins (margins_kernel)",
+             "attn": "cure_tree_attn (tree_attn_mfma + attn_merge)",
+             "accept": "cure_accept (accept_kernel)"}
+    value = step_bytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "ctx_len": int(w.ctx_len.max()),
+                   "tree_nodes": int(w.n_nodes.max()), "hq": w.hq, "hkv": w.hkv, "d": w.d,
+                   "vocab": w.vocab, "chain_len": w.chain_len, "repair_budget": w.repair_budget,
+                   "parallelism": "single-gpu", "input_copies": ncopy},
+        "step_latency_us": round(ms * 1e3, 2),
+        "kv_gbps": round(ab["attention_kv"] / (calls["attn"] * 1e-6) / 1e9, 1),
+        "event_ms_per_step": round(ev_ms, 5),
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "kernel": names[dom], "achieved": round(dom_gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

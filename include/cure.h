@@ -1,0 +1,179 @@
+/*
+ * libcure -- MI355X (gfx950) verify-and-repair hot path of CURE
+ * (local uncertainty repair for block-parallel speculative decoding).
+ *
+ * Three stream-ordered entry points cover one decoding iteration's data-parallel
+ * work on the device:
+ *
+ *   cure_margins    top-1/top-2 margin and log-sum-exp per logits row, plus the
+ *                   Uncertainty Focal Point (UFP) selection      (Sec. 3.3, Eq. 2)
+ *   cure_tree_attn  tree-masked verification attention over the KV cache and
+ *                   each node's own tree ancestors           (Sec. 3.2, 3.4, 3.5)
+ *   cure_accept     accepted prefix per path and the best path     (Eq. 1, Eq. 4)
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers (memory the caller allocated with
+ *    hipMalloc or equivalent), except those whose name starts with host_.
+ *    The library allocates no device memory and keeps no state beyond a cached
+ *    device-property query; the caller owns every buffer.
+ *  - stream is a hipStream_t passed as void* (NULL = the legacy default stream).
+ *    Calls only enqueue work: they return before the work runs, and the outputs
+ *    are valid once the stream reaches that point.
+ *  - The return value reports errors the host can see: invalid arguments,
+ *    unsupported shapes, a too-small workspace and HIP launch failures. Errors
+ *    in device data (a malformed tree) are reported through device status words.
+ *    No C++ exception crosses this interface.
+ *  - Workspaces: a call that takes a workspace needs at least the size its
+ *    *_workspace_size function returns for the same arguments (0 means none is
+ *    needed and the pointer may be NULL). A workspace holds scratch data only
+ *    while the call's kernels run: it needs no initialisation and may be reused
+ *    by any later call on the same stream. Two calls whose work may overlap on
+ *    the GPU must not share a workspace.
+ *  - bf16 values are raw IEEE bfloat16 bit patterns (uint16 storage).
+ */
+#ifndef CURE_H
+#define CURE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cure_status {
+  CURE_OK = 0,
+  CURE_ERR_INVALID_ARG = 1,   /* null pointer, negative size, inconsistent shapes   */
+  CURE_ERR_UNSUPPORTED = 2,   /* shape outside what the kernels implement            */
+  CURE_ERR_BAD_TREE = 3,      /* device status word only: parent[n] not in [-1, n-1] */
+  CURE_ERR_HIP = 4,           /* a HIP runtime call or kernel launch failed          */
+  CURE_ERR_WORKSPACE = 5      /* workspace null or smaller than required             */
+} cure_status;
+
+typedef enum cure_dtype { CURE_F32 = 0, CURE_BF16 = 1 } cure_dtype;
+
+/* Flags for cure_tree_attn. */
+#define CURE_ATTN_FORCE_VALU 1u   /* use the vector-ALU kernel even where MFMA applies */
+
+#define CURE_MAX_TREE_NODES 256   /* largest tree (nodes per sequence) supported       */
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* cure_status_string(int status);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int cure_version(void);
+
+/* ------------------------------------------------------------------------- */
+/* Margin pass and UFP gate -- Sec. 3.3 Eq. (2) and Algorithm 1.
+ *
+ * For every row r of logits (batch*rows rows of vocab entries; row r of
+ * sequence b starts at element (b*rows + r)*ld):
+ *   top1_idx/top1_val  the largest entry,
+ *   top2_idx/top2_val  the next entry in the order (value descending, index
+ *                      ascending) -- ties go to the lowest index, so a maximum
+ *                      that occurs twice gives top2 = its second index,
+ *   margin             top1_val - top2_val, computed in float32,
+ *   lse                log(sum_v exp(x_v)), natural log, float32.
+ * Entries are widened exactly to float32; values must be finite or -inf.
+ *
+ * UFP gate (skipped when ufp_pos and ufp_cnt are both NULL): over the first
+ * chain_len rows of each sequence, the positions with margin < tau (strict),
+ * ordered by (margin ascending, position ascending), at most
+ * floor(repair_budget / branch_depth) of them, so that branches of branch_depth
+ * nodes never exceed the repair budget. ufp_pos is [batch][chain_len] int32,
+ * filled with the selected positions in that order and padded with -1;
+ * ufp_cnt is [batch] int32.
+ *
+ * Layout: logits row-major, ld >= vocab elements between rows; every per-row
+ * output has batch*rows entries. Requires vocab >= 2, 0 <= chain_len <= rows
+ * (chain_len >= 1 when the gate runs), branch_depth >= 1, repair_budget >= 0.
+ * workspace: cure_margins_workspace_size(batch, rows, vocab) bytes.
+ */
+size_t cure_margins_workspace_size(int32_t batch, int32_t rows, int32_t vocab);
+
+cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
+                         int32_t vocab, int64_t ld,
+                         float* top1_val, int32_t* top1_idx, float* top2_val,
+                         int32_t* top2_idx, float* lse, float* margin,
+                         int32_t chain_len, float tau, int32_t repair_budget,
+                         int32_t branch_depth, int32_t* ufp_pos, int32_t* ufp_cnt,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Tree-attention verification -- Sec. 3.2 (phase 3), Sec. 3.4, Sec. 3.5.
+ *
+ * One forward attention layer of the target over every node of each
+ * sequence's candidate tree. Node n of sequence b, query head h (key/value head
+ * h / (hq/hkv)) attends to
+ *   - the ctx_len[b] cached context rows, and
+ *   - the tree rows of the nodes on its own root path, itself included,
+ * with scores scale * <q, k>, natural-base softmax:
+ *   o[b][n][h]   = sum_j softmax_j * v_j            (normalised)
+ *   lse[b][n][h] = log sum_j exp(scale * <q, k_j>)
+ *
+ * Layout:
+ *   q       [batch][n_max][hq][d]          dtype
+ *   k, v    token rows of [hkv][d]         dtype; sequence b owns rows
+ *           kv_off[b] .. kv_off[b] + ctx_len[b] + n_nodes[b] - 1: its context,
+ *           then its tree nodes in node order
+ *   o       [batch][n_max][hq][d]          out_dtype (CURE_F32 or CURE_BF16)
+ *   lse     [batch][n_max][hq]             float32 (may be NULL)
+ *   parent  [batch][n_max]                 int32, parent[n] in [-1, n-1]: the
+ *           tree in topological order, -1 = attached to the context
+ *   kv_off  [batch] int64, ctx_len/n_nodes [batch] int32 (device)
+ *   host_ctx_len/host_n_nodes: host copies of ctx_len/n_nodes, used only to
+ *           plan the split of each context across workgroups.
+ * Rows n >= n_nodes[b] of o and lse are not written.
+ * tree_status [batch] int32 (may be NULL): CURE_OK, or CURE_ERR_BAD_TREE when
+ * sequence b's parent array is malformed (that sequence's o/lse are then
+ * unspecified).
+ * Supports d in {64, 128}, hq % hkv == 0, 0 <= n_nodes[b] <= min(n_max, 256)
+ * (a sequence with no nodes is skipped).
+ * kv_split: 0 = automatic, else the number of context splits per sequence.
+ * flags: CURE_ATTN_FORCE_VALU or 0.
+ * workspace: cure_tree_attn_workspace_size(...) bytes for the same arguments.
+ */
+size_t cure_tree_attn_workspace_size(int32_t batch, int32_t hq, int32_t hkv, int32_t d,
+                                     int32_t n_max, const int32_t* host_ctx_len,
+                                     const int32_t* host_n_nodes, int32_t kv_split);
+
+cure_status cure_tree_attn(const void* q, const void* k, const void* v, void* o, float* lse,
+                           int32_t dtype, int32_t out_dtype, int32_t batch, int32_t hq,
+                           int32_t hkv, int32_t d, float scale, const int64_t* kv_off,
+                           const int32_t* ctx_len, const int32_t* n_nodes,
+                           const int32_t* parent, int32_t n_max,
+                           const int32_t* host_ctx_len, const int32_t* host_n_nodes,
+                           int32_t kv_split, uint32_t flags, int32_t* tree_status,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Acceptance walk -- Sec. 3.1 Eq. (1), Sec. 3.5 Eq. (4), greedy decoding.
+ *
+ * Per sequence b with n_nodes[b] nodes (all arrays [batch][n_max] int32 unless
+ * noted):
+ *   node n is accepted when its token equals the target's argmax before it --
+ *   root_tgt[b] for parent[n] == -1, else tgt[parent[n]] -- and its parent is
+ *   accepted. The winner is the accepted node of greatest depth, lowest index
+ *   on ties (so branch 0, numbered first, wins ties).
+ *   acc_len [batch]  depth(winner)+1, or 0 when nothing is accepted
+ *   best    [batch]  the winner, or -1
+ *   path    [batch][n_max] root->winner node indices, padded with -1
+ *   bonus   [batch]  tgt[winner], or root_tgt[b] when nothing is accepted
+ *   resync  [batch]  1 when the winning path holds a node >= chain_len (a repair
+ *                    node, so the draft cache must be resynchronised), else 0;
+ *                    -1 together with acc_len = -1 when the parent array is
+ *                    malformed.
+ * tgt is typically cure_margins' top1_idx over the target's node logits.
+ * Supports 0 <= n_nodes[b] <= min(n_max, 256); with no nodes, acc_len = 0
+ * and bonus = root_tgt.
+ */
+cure_status cure_accept(const int32_t* parent, const int32_t* token, const int32_t* tgt,
+                        const int32_t* root_tgt, const int32_t* n_nodes, int32_t chain_len,
+                        int32_t batch, int32_t n_max, int32_t* acc_len, int32_t* path,
+                        int32_t* best, int32_t* bonus, int32_t* resync, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CURE_H */

@@ -1,0 +1,444 @@
+// cure_margins: one streaming pass over each logits row computing the top-1 /
+// top-2 entries, the log-sum-exp and the predictive confidence margin
+// (Sec. 3.3, Eq. 2), plus the UFP selection of Algorithm 1 as an epilogue.
+//
+// Work decomposition: each row is cut into `splits` contiguous chunks, one
+// 256-thread workgroup per (row, chunk). A lane reads 16-byte vectors of 8
+// entries and keeps an online log-sum-exp plus its two best vectors ranked by
+// (vector maximum descending, position ascending). A lane's top-2 entries
+// always lie in those two vectors: the top-1 sits in the first vector holding
+// the largest value, and the top-2 is either beside it or is the maximum of the
+// best other vector. So the streaming loop tracks vectors branch-free (their
+// raw bits stay in registers), and only at the end does each lane rank those
+// 16 entries exactly (value descending, index ascending).
+//
+// With one chunk per row the workgroup writes the row's results itself. With
+// several, chunk results go to the workspace and margins_finish (one workgroup
+// per sequence) merges them with an associative (value desc, index asc) top-2
+// merge; the same kernel runs the UFP selection. Workgroups never wait on each
+// other inside a kernel: on a multi-die GPU the device-scope fences such a
+// hand-off needs cost far more than a second, tiny launch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "common.hpp"
+#include "host_util.hpp"
+
+namespace cure {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kVec = 8;            // entries per lane per vector step
+constexpr int kUnroll = 2;         // vector steps per lane per loop step
+constexpr int kMaxSplits = 32;
+constexpr int kMinChunk = 8192;    // entries per workgroup, at least
+constexpr int kTargetWgsPerCu = 2;
+constexpr int kMaxGateChain = 1024;
+constexpr float kRescaleAt = 16.f; // re-reference the exp sum when a value exceeds ref + 16
+
+struct Partial {
+  float ref, sum, v1, v2;
+  int32_t i1, i2, pad0, pad1;
+};
+static_assert(sizeof(Partial) == 32, "partial record is 32 bytes");
+
+struct Args {
+  const void* logits;
+  int64_t ld;
+  int32_t rows, vocab, splits, chunk, iters;
+  float* top1_val;
+  int32_t* top1_idx;
+  float* top2_val;
+  int32_t* top2_idx;
+  float* lse;
+  float* margin;
+  int32_t chain_len, max_ufp;
+  float tau;
+  int32_t* ufp_pos;
+  int32_t* ufp_cnt;
+  Partial* partials;     // [rows total][splits], only when splits > 1
+};
+
+// Raw buffer loads: the chunk is described by a buffer resource (base, size),
+// lane offsets are 32-bit and the per-step offset is a scalar, so the loop
+// carries no 64-bit address arithmetic. Reads at or past the resource's size
+// return zero instead of touching memory.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kRsrcWord3 = 0x00020000;   // raw (untyped) 32-bit access, gfx9 family
+
+CURE_DEV __amdgpu_buffer_rsrc_t chunk_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
+}
+
+// One lane's 8 entries as raw registers, then widened.
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<uint16_t> {
+  u32x4 w;
+  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t step_off) {
+    w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)step_off, 0);
+  }
+  static constexpr uint32_t kBytes = 16;
+  CURE_DEV void widen(float (&f)[kVec]) const {
+    f[0] = bf16_lo(w.x); f[1] = bf16_hi(w.x);
+    f[2] = bf16_lo(w.y); f[3] = bf16_hi(w.y);
+    f[4] = bf16_lo(w.z); f[5] = bf16_hi(w.z);
+    f[6] = bf16_lo(w.w); f[7] = bf16_hi(w.w);
+  }
+};
+template <>
+struct Raw8<float> {
+  u32x4 a, b;
+  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t step_off) {
+    a = __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)step_off, 0);
+    b = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(lane_off + 16), (int)step_off, 0);
+  }
+  static constexpr uint32_t kBytes = 32;
+  CURE_DEV void widen(float (&f)[kVec]) const {
+    f[0] = __uint_as_float(a.x); f[1] = __uint_as_float(a.y);
+    f[2] = __uint_as_float(a.z); f[3] = __uint_as_float(a.w);
+    f[4] = __uint_as_float(b.x); f[5] = __uint_as_float(b.y);
+    f[6] = __uint_as_float(b.z); f[7] = __uint_as_float(b.w);
+  }
+};
+
+// Three-input maximum on the VALU. The inputs are never NaN (the interface
+// excludes NaN logits), so no quieting of the operands is needed.
+CURE_DEV float max3(float a, float b, float c) {
+  float r;
+  asm volatile("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+CURE_DEV float max8(const float (&f)[kVec]) {
+  return max3(max3(f[0], f[1], f[2]), max3(f[3], f[4], f[5]), max3(f[6], f[7], f[7]));
+}
+
+template <typename T>
+CURE_DEV float load1(const T* p);
+template <>
+CURE_DEV float load1<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+template <>
+CURE_DEV float load1<float>(const float* p) { return *p; }
+
+CURE_DEV void write_row(const Args& a, int row, const Top2& t, float lse) {
+  a.top1_val[row] = t.v1;
+  a.top1_idx[row] = t.i1;
+  a.top2_val[row] = t.v2;
+  a.top2_idx[row] = t.i2;
+  a.lse[row] = lse;
+  a.margin[row] = t.v1 - t.v2;
+}
+
+// UFP selection for sequence b: candidates m < tau, ranked by (m, position).
+CURE_DEV void select_ufp(const Args& a, int b, float* sm) {
+  const int K = a.chain_len;
+  for (int i = threadIdx.x; i < K; i += kThreads) sm[i] = a.margin[(int64_t)b * a.rows + i];
+  __syncthreads();
+  int local = 0;
+  for (int i = threadIdx.x; i < K; i += kThreads) {
+    const float mi = sm[i];
+    if (!(mi < a.tau)) continue;
+    ++local;
+    int rank = 0;
+    for (int j = 0; j < K; ++j) {
+      const float mj = sm[j];
+      rank += (mj < a.tau) && (mj < mi || (mj == mi && j < i));
+    }
+    if (rank < a.max_ufp) a.ufp_pos[(int64_t)b * K + rank] = i;
+  }
+  // Count candidates across the block.
+  __shared__ int s_cnt;
+  if (threadIdx.x == 0) s_cnt = 0;
+  __syncthreads();
+  if (local) atomicAdd(&s_cnt, local);
+  __syncthreads();
+  const int cnt = min(s_cnt, a.max_ufp);
+  for (int p = cnt + threadIdx.x; p < K; p += kThreads) a.ufp_pos[(int64_t)b * K + p] = -1;
+  if (threadIdx.x == 0) a.ufp_cnt[b] = cnt;
+}
+
+template <typename T, bool kVecPath>
+__global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
+  __shared__ Top2 s_top[kThreads / kWave];
+  __shared__ Lse s_lse[kThreads / kWave];
+
+  const int row = blockIdx.x / a.splits;
+  const int split = blockIdx.x - row * a.splits;
+  const T* x = reinterpret_cast<const T*>(a.logits) + (int64_t)row * a.ld;
+  const int begin = split * a.chunk;
+  const int end = min(a.vocab, begin + a.chunk);
+  const int tid = threadIdx.x;
+
+  Top2 t = top2_empty();
+  float ref = kLseEmptyRef, sum = 0.f;
+  float nref = -ref * kLog2e;
+
+  int scalar_from = begin;
+  if (kVecPath) {
+    const int nvec = (end - begin) / kVec;
+    scalar_from = begin + nvec * kVec;
+    // The lane's two best vectors (index within the chunk, -1 = none).
+    float bm1 = -INFINITY, bm2 = -INFINITY;
+    Raw8<T> kr1, kr2;                    // raw entries of those two vectors
+    int bv1 = -1, bv2 = -1;
+    if (nvec > 0) {
+      // Lanes past the chunk's last vector read zeros (outside the buffer
+      // resource) and ignore them, so every load is unconditional. Two register
+      // sets alternate: one step's loads are in flight while the previous step
+      // is processed.
+      const __amdgpu_buffer_rsrc_t rsrc = chunk_rsrc(x + begin, (uint32_t)nvec * Raw8<T>::kBytes);
+      const uint32_t lane_off = (uint32_t)tid * Raw8<T>::kBytes;
+      Raw8<T> ra[kUnroll], rb[kUnroll];
+      auto issue = [&](Raw8<T>(&r)[kUnroll], int it) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+          r[u].load(rsrc, lane_off, (uint32_t)((it * kUnroll + u) * kThreads) * Raw8<T>::kBytes);
+      };
+      auto process = [&](const Raw8<T>(&r)[kUnroll], int it) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int v = (it * kUnroll + u) * kThreads + tid;
+          const bool ok = v < nvec;
+          float f[kVec];
+          r[u].widen(f);
+          const float m8 = ok ? max8(f) : -INFINITY;
+          // Best-two-vectors update. The lane's first vector is taken even if it
+          // is all -inf, so a lane with data always has a best vector.
+          const bool c1 = ok && (m8 > bm1 || bv1 < 0);
+          const bool c2 = ok && !c1 && m8 > bm2;
+          bm2 = c1 ? bm1 : (c2 ? m8 : bm2);
+          bv2 = c1 ? bv1 : (c2 ? v : bv2);
+          if (c1) kr2 = kr1;
+          if (c2) kr2 = r[u];
+          if (c1) kr1 = r[u];
+          bm1 = c1 ? m8 : bm1;
+          bv1 = c1 ? v : bv1;
+          // Log-sum-exp against a lagging reference, moved only on large jumps.
+          const bool resc = m8 > ref + kRescaleAt;
+          if (__builtin_expect(__ballot(resc) != 0, 0)) {
+            if (resc) {
+              sum *= fast_exp2((ref - m8) * kLog2e);
+              ref = m8;
+              nref = -ref * kLog2e;
+            }
+          }
+          if (ok) {
+            float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+            for (int j = 0; j < kVec; j += 2) {
+              s0 += fast_exp2(fmaf(f[j], kLog2e, nref));
+              s1 += fast_exp2(fmaf(f[j + 1], kLog2e, nref));
+            }
+            sum += s0 + s1;
+          }
+        }
+      };
+      // Prefetches past the last step fall outside the resource and read zeros,
+      // so they need no guard and the waits before each step stay partial.
+      issue(ra, 0);
+      for (int it = 0; it < a.iters; it += 2) {
+        issue(rb, it + 1);
+        process(ra, it);
+        if (it + 1 >= a.iters) break;
+        issue(ra, it + 2);
+        process(rb, it + 1);
+      }
+    }
+    // Exact top-2 over the entries of the lane's two best vectors.
+    if (bv1 >= 0) {
+      float f[kVec];
+      kr1.widen(f);
+#pragma unroll
+      for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + bv1 * kVec + j);
+      if (bv2 >= 0) {
+        kr2.widen(f);
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + bv2 * kVec + j);
+      }
+    }
+  }
+  for (int i = scalar_from + tid; i < end; i += kThreads) {
+    const float xv = load1<T>(x + i);
+    top2_push(t, xv, i);
+    if (xv > ref + kRescaleAt) {
+      sum *= fast_exp2((ref - xv) * kLog2e);
+      ref = xv;
+      nref = -ref * kLog2e;
+    }
+    sum += fast_exp2(fmaf(xv, kLog2e, nref));
+  }
+
+  // Workgroup reduction.
+  t = top2_wave_reduce(t);
+  Lse s = lse_wave_reduce(Lse{ref, sum});
+  const int wave = tid / kWave;
+  if ((tid & (kWave - 1)) == 0) { s_top[wave] = t; s_lse[wave] = s; }
+  __syncthreads();
+
+  // Chunk result of this workgroup (thread 0 combines the wave results).
+  if (tid == 0) {
+    Top2 bt = s_top[0];
+    Lse bs = s_lse[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / kWave; ++w) {
+      bt = top2_merge(bt, s_top[w]);
+      bs = lse_merge(bs, s_lse[w]);
+    }
+    if (a.splits > 1) {
+      a.partials[(int64_t)row * a.splits + split] =
+          Partial{bs.ref, bs.sum, bt.v1, bt.v2, bt.i1, bt.i2, 0, 0};
+    } else {
+      write_row(a, row, bt, lse_value(bs));
+    }
+  }
+}
+
+// Per sequence: merge each row's chunk results (when rows were split), then
+// select the sequence's UFPs from its chain rows' margins.
+//
+// Lanes are grouped G = splits rounded up to a power of two: each group holds
+// one row's chunk results, one per lane, and reduces them with xor shuffles
+// inside the group. kFinishUnroll passes of rows are loaded before any is
+// reduced, so a sequence costs one memory round trip per 4 * kFinishUnroll *
+// (64 / G) rows.
+constexpr int kFinishUnroll = 4;
+
+CURE_DEV Top2 top2_group_reduce(Top2 t, int group) {
+  for (int m = group >> 1; m >= 1; m >>= 1) {
+    Top2 o;
+    o.v1 = shfl_xor(t.v1, m); o.i1 = shfl_xor(t.i1, m);
+    o.v2 = shfl_xor(t.v2, m); o.i2 = shfl_xor(t.i2, m);
+    t = top2_merge(t, o);
+  }
+  return t;
+}
+
+CURE_DEV Lse lse_group_reduce(Lse s, int group) {
+  for (int m = group >> 1; m >= 1; m >>= 1) s = lse_merge(s, Lse{shfl_xor(s.ref, m), shfl_xor(s.sum, m)});
+  return s;
+}
+
+__global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
+  __shared__ float s_margin[kMaxGateChain];
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  if (a.splits > 1) {
+    int group = 1;
+    while (group < a.splits) group <<= 1;               // splits <= kMaxSplits <= 64
+    const int per_wave = kWave / group;
+    const int per_pass = per_wave * (kThreads / kWave);
+    const int sp = lane & (group - 1);
+    const int r_in_pass = wave * per_wave + lane / group;
+    for (int r0 = 0; r0 < a.rows; r0 += per_pass * kFinishUnroll) {
+      Partial q[kFinishUnroll];
+#pragma unroll
+      for (int u = 0; u < kFinishUnroll; ++u) {
+        const int r = r0 + u * per_pass + r_in_pass;
+        q[u] = Partial{kLseEmptyRef, 0.f, -INFINITY, -INFINITY, INT32_MAX, INT32_MAX, 0, 0};
+        if (r < a.rows && sp < a.splits)
+          q[u] = a.partials[((int64_t)b * a.rows + r) * a.splits + sp];
+      }
+#pragma unroll
+      for (int u = 0; u < kFinishUnroll; ++u) {
+        const int r = r0 + u * per_pass + r_in_pass;
+        const Top2 t = top2_group_reduce(Top2{q[u].v1, q[u].v2, q[u].i1, q[u].i2}, group);
+        const Lse ls = lse_group_reduce(Lse{q[u].ref, q[u].sum}, group);
+        if (sp == 0 && r < a.rows) write_row(a, b * a.rows + r, t, lse_value(ls));
+      }
+    }
+    if (a.ufp_pos) {
+      __threadfence_block();
+      __syncthreads();
+    }
+  }
+  if (a.ufp_pos) select_ufp(a, b, s_margin);
+}
+
+}  // namespace
+}  // namespace cure
+
+using namespace cure;
+
+extern "C" size_t cure_margins_workspace_size(int32_t batch, int32_t rows, int32_t vocab) {
+  (void)vocab;
+  if (batch <= 0 || rows <= 0) return 0;
+  return align_up((size_t)batch * rows * kMaxSplits * sizeof(Partial), 256);
+}
+
+extern "C" cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch,
+                                    int32_t rows, int32_t vocab, int64_t ld, float* top1_val,
+                                    int32_t* top1_idx, float* top2_val, int32_t* top2_idx,
+                                    float* lse, float* margin, int32_t chain_len, float tau,
+                                    int32_t repair_budget, int32_t branch_depth,
+                                    int32_t* ufp_pos, int32_t* ufp_cnt, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (dtype != CURE_F32 && dtype != CURE_BF16) return CURE_ERR_INVALID_ARG;
+  if (batch < 0 || rows < 0) return CURE_ERR_INVALID_ARG;
+  if (batch == 0 || rows == 0) return CURE_OK;
+  if (vocab < 2 || ld < vocab) return CURE_ERR_INVALID_ARG;
+  if (!logits || !top1_val || !top1_idx || !top2_val || !top2_idx || !lse || !margin)
+    return CURE_ERR_INVALID_ARG;
+  const bool gate = ufp_pos != nullptr || ufp_cnt != nullptr;
+  if (gate) {
+    if (!ufp_pos || !ufp_cnt) return CURE_ERR_INVALID_ARG;
+    if (chain_len < 1 || chain_len > rows || branch_depth < 1 || repair_budget < 0)
+      return CURE_ERR_INVALID_ARG;
+    if (chain_len > kMaxGateChain) return CURE_ERR_UNSUPPORTED;
+  }
+  const int64_t nrow = (int64_t)batch * rows;
+  if (nrow > INT32_MAX / kMaxSplits) return CURE_ERR_UNSUPPORTED;
+
+  // Enough workgroups to cover the GPU several times over, each chunk at
+  // least kMinChunk entries.
+  int splits = (int)((kTargetWgsPerCu * (int64_t)device_cu_count() + nrow - 1) / nrow);
+  splits = std::max(1, std::min(splits, std::min(kMaxSplits, vocab / kMinChunk)));
+  int chunk = (vocab + splits - 1) / splits;
+  chunk = (chunk + kVec - 1) / kVec * kVec;
+  splits = (vocab + chunk - 1) / chunk;
+  if (splits > 1 &&
+      (!workspace || workspace_bytes < cure_margins_workspace_size(batch, rows, vocab)))
+    return CURE_ERR_WORKSPACE;
+
+  const size_t esize = dtype == CURE_F32 ? 4 : 2;
+  const bool vec_ok = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
+                      ((size_t)ld * esize) % 16 == 0;
+
+  Args a;
+  a.logits = logits;
+  a.ld = ld;
+  a.rows = rows;
+  a.vocab = vocab;
+  a.splits = splits;
+  a.chunk = chunk;
+  const int per_iter = kThreads * kVec * kUnroll;
+  a.iters = (chunk + per_iter - 1) / per_iter;
+  a.top1_val = top1_val;
+  a.top1_idx = top1_idx;
+  a.top2_val = top2_val;
+  a.top2_idx = top2_idx;
+  a.lse = lse;
+  a.margin = margin;
+  a.chain_len = gate ? chain_len : 0;
+  a.max_ufp = gate ? repair_budget / branch_depth : 0;
+  a.tau = tau;
+  a.ufp_pos = gate ? ufp_pos : nullptr;
+  a.ufp_cnt = gate ? ufp_cnt : nullptr;
+  a.partials = reinterpret_cast<Partial*>(workspace);
+
+  const dim3 grid((unsigned)(nrow * splits)), block(kThreads);
+  hipStream_t s = as_stream(stream);
+  if (dtype == CURE_BF16) {
+    if (vec_ok) hipLaunchKernelGGL((margins_kernel<uint16_t, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((margins_kernel<uint16_t, false>), grid, block, 0, s, a);
+  } else {
+    if (vec_ok) hipLaunchKernelGGL((margins_kernel<float, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((margins_kernel<float, false>), grid, block, 0, s, a);
+  }
+  if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
+  if (splits > 1 || gate)
+    hipLaunchKernelGGL(margins_finish, dim3(batch), block, 0, s, a);
+  return launch_status();
+}

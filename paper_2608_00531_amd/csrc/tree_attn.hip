@@ -1,0 +1,735 @@
+// cure_tree_attn: tree-masked verification attention (Sec. 3.2 phase 3,
+// Sec. 3.4, Sec. 3.5) as a split-KV ("flash-decoding") pass plus a
+// log-sum-exp merge of the split partials.
+//
+// Every node of a sequence's candidate tree attends to the whole cached
+// context and to the nodes on its own root path. The context is shared by all
+// nodes, so the work is organised around the key/value stream: one workgroup
+// owns (sequence, kv-head, row block, context split) and reads each K/V tile
+// from HBM exactly once for all query rows of that kv-head -- the G query heads
+// of every tree node, packed node-major. Only tiles that reach the tree rows
+// at the tail of the sequence apply the ancestor bitmask.
+//
+// Two kernels compute a split:
+//  * tree_attn_mfma: bf16, head dim 64/128. Scores are formed transposed,
+//    S^T = K Q^T, and the output as O^T = V^T P^T with 32x32x16 bf16 MFMAs, so
+//    each lane owns one query row and the online softmax needs no cross-lane
+//    traffic beyond one swap between the two half-waves. V is staged in LDS
+//    transposed (token-minor) with the token order inside each 16-token group
+//    permuted to match where the score MFMA leaves P in registers.
+//  * tree_attn_valu: fp32 or bf16, any supported shape; plain vector ALU code.
+// A split writes normalised partial O and its log-sum-exp; attn_merge combines
+// the splits of each row (skipped when a sequence has a single split, in which
+// case the split kernel writes the final output itself).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "common.hpp"
+#include "host_util.hpp"
+
+namespace cure {
+namespace {
+
+constexpr int kTile = 64;            // tokens per K/V tile
+constexpr int kMinTps = 256;         // tokens per split, at least
+constexpr int kAncWords = CURE_MAX_TREE_NODES / 64;
+
+struct Args {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  int32_t out_bf16;
+  int32_t hq, hkv, group, n_max;
+  float scale_log2;                  // scale * log2(e): scores live in the log2 domain
+  const int64_t* kv_off;
+  const int32_t* ctx_len;
+  const int32_t* n_nodes;
+  const int32_t* parent;
+  int32_t tps, max_splits, rows_per_wg;
+  int32_t* tree_status;
+  float* part_o;                     // [batch][hq][n_max][max_splits][d]
+  float* part_lse;                   // [batch][hq][n_max][max_splits]
+};
+
+// Number of context splits of a sequence with T = ctx + nodes rows. The last
+// split runs to T, so a clamp never drops rows.
+CURE_DEV int split_count(int T, int N, int tps, int max_splits) {
+  if (N <= 0 || T <= 0) return 0;
+  return min((T + tps - 1) / tps, max_splits);
+}
+
+CURE_DEV int64_t part_index(const Args& a, int b, int head, int n, int s) {
+  return (((int64_t)b * a.hq + head) * a.n_max + n) * a.max_splits + s;
+}
+
+// Loads sequence b's parent array, validates it and builds every node's
+// ancestor bitmask (its root path, itself included). Returns true if valid.
+CURE_DEV bool build_tree(const Args& a, int b, int N, int* s_parent,
+                         unsigned long long (*s_anc)[kAncWords], int* s_bad) {
+  if (threadIdx.x == 0) *s_bad = 0;
+  __syncthreads();
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    const int p = a.parent[(int64_t)b * a.n_max + n];
+    s_parent[n] = p;
+    if (p < -1 || p >= n) *s_bad = 1;
+  }
+  __syncthreads();
+  if (*s_bad) return false;
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    unsigned long long w[kAncWords] = {};
+    for (int j = n; j >= 0; j = s_parent[j]) w[j >> 6] |= 1ull << (j & 63);
+#pragma unroll
+    for (int i = 0; i < kAncWords; ++i) s_anc[n][i] = w[i];
+  }
+  __syncthreads();
+  return true;
+}
+
+CURE_DEV void report_tree(const Args& a, int b, bool ok, bool reporter) {
+  if (reporter && threadIdx.x == 0 && a.tree_status) a.tree_status[b] = ok ? CURE_OK : CURE_ERR_BAD_TREE;
+}
+
+// Visibility of cache row tok (relative to the sequence) for node n.
+CURE_DEV bool visible(int tok, int L, int N, int n, const unsigned long long (*s_anc)[kAncWords]) {
+  if (tok < L) return true;
+  const int j = tok - L;
+  if (j >= N) return false;
+  return (s_anc[n][j >> 6] >> (j & 63)) & 1ull;
+}
+
+template <typename T>
+CURE_DEV float ld_elem(const T* p);
+template <>
+CURE_DEV float ld_elem<float>(const float* p) { return *p; }
+template <>
+CURE_DEV float ld_elem<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+CURE_DEV void store_out(const Args& a, int64_t idx, float val) {
+  if (a.out_bf16) reinterpret_cast<uint16_t*>(a.o)[idx] = f32_to_bf16(val);
+  else reinterpret_cast<float*>(a.o)[idx] = val;
+}
+
+// ---------------------------------------------------------------------------
+// Vector-ALU split kernel: 4 waves, 8 query rows per wave, one token per lane
+// for the scores and D/64 output columns per lane for P V.
+constexpr int kValuRowsPerWave = 8;
+constexpr int kValuWaves = 4;
+constexpr int kValuRows = kValuRowsPerWave * kValuWaves;
+
+template <typename E, int D>
+__global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
+  __shared__ int s_parent[CURE_MAX_TREE_NODES];
+  __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
+  __shared__ int s_bad;
+  __shared__ float s_q[kValuRows][D];
+  __shared__ float s_k[kTile][D + 1];
+  __shared__ float s_v[kTile][D];
+  __shared__ float s_p[kValuWaves][kValuRowsPerWave][kTile];
+
+  const int b = blockIdx.z;
+  const int hk = blockIdx.y % a.hkv;
+  const int rb = blockIdx.y / a.hkv;
+  const int s = blockIdx.x;
+  const int N = min(a.n_nodes[b], a.n_max);
+  const int L = a.ctx_len[b];
+  const int T = L + N;
+  const int S = split_count(T, N, a.tps, a.max_splits);
+  const int rows = N * a.group;
+  if (s >= S || rb * kValuRows >= rows) return;
+  const bool reporter = s == 0 && hk == 0 && rb == 0;
+  const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
+  report_tree(a, b, ok, reporter);
+  if (!ok) return;
+
+  const int begin = s * a.tps;
+  const int end = (s == S - 1) ? T : begin + a.tps;
+  const int64_t off = a.kv_off[b];
+  const E* qp = reinterpret_cast<const E*>(a.q);
+  const E* kp = reinterpret_cast<const E*>(a.k);
+  const E* vp = reinterpret_cast<const E*>(a.v);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  for (int i = tid; i < kValuRows * D; i += 256) {
+    const int r = i / D, d = i - r * D;
+    const int R = rb * kValuRows + r;
+    float val = 0.f;
+    if (R < rows) {
+      const int n = R / a.group, head = hk * a.group + R % a.group;
+      val = ld_elem<E>(qp + (((int64_t)b * a.n_max + n) * a.hq + head) * D + d);
+    }
+    s_q[r][d] = val;
+  }
+
+  float m_run[kValuRowsPerWave], l_run[kValuRowsPerWave], acc[kValuRowsPerWave][D / 64];
+#pragma unroll
+  for (int i = 0; i < kValuRowsPerWave; ++i) {
+    m_run[i] = -INFINITY;
+    l_run[i] = 0.f;
+#pragma unroll
+    for (int c = 0; c < D / 64; ++c) acc[i][c] = 0.f;
+  }
+
+  for (int t0 = begin; t0 < end; t0 += kTile) {
+    __syncthreads();
+    for (int i = tid; i < kTile * D; i += 256) {
+      const int t = i / D, d = i - t * D;
+      const int tok = t0 + t;
+      float kv = 0.f, vv = 0.f;
+      if (tok < end) {
+        const int64_t e = ((off + tok) * a.hkv + hk) * D + d;
+        kv = ld_elem<E>(kp + e);
+        vv = ld_elem<E>(vp + e);
+      }
+      s_k[t][d] = kv;
+      s_v[t][d] = vv;
+    }
+    __syncthreads();
+
+    // Scores for this wave's rows: lane = token.
+    float sc[kValuRowsPerWave];
+#pragma unroll
+    for (int i = 0; i < kValuRowsPerWave; ++i) sc[i] = 0.f;
+    for (int d = 0; d < D; ++d) {
+      const float kd = s_k[lane][d];
+#pragma unroll
+      for (int i = 0; i < kValuRowsPerWave; ++i)
+        sc[i] = fmaf(s_q[wave * kValuRowsPerWave + i][d], kd, sc[i]);
+    }
+    const int tok = t0 + lane;
+#pragma unroll
+    for (int i = 0; i < kValuRowsPerWave; ++i) {
+      const int R = rb * kValuRows + wave * kValuRowsPerWave + i;
+      const int n = min(R / a.group, N - 1);
+      const bool vis = tok < end && visible(tok, L, N, n, s_anc);
+      const float x = vis ? sc[i] * a.scale_log2 : -INFINITY;
+      float mt = x;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) mt = fmaxf(mt, shfl_xor(mt, m));
+      const float m_new = fmaxf(m_run[i], mt);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float p = exp2f(x - m_use);
+      float ps = p;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) ps += shfl_xor(ps, m);
+      const float alpha = exp2f(m_run[i] - m_use);
+      l_run[i] = l_run[i] * alpha + ps;
+      m_run[i] = m_new;
+#pragma unroll
+      for (int c = 0; c < D / 64; ++c) acc[i][c] *= alpha;
+      s_p[wave][i][lane] = p;
+    }
+    // P V: lane = output column(s).
+    for (int t = 0; t < kTile; ++t) {
+      float vv[D / 64];
+#pragma unroll
+      for (int c = 0; c < D / 64; ++c) vv[c] = s_v[t][lane + 64 * c];
+#pragma unroll
+      for (int i = 0; i < kValuRowsPerWave; ++i) {
+        const float p = s_p[wave][i][t];
+#pragma unroll
+        for (int c = 0; c < D / 64; ++c) acc[i][c] = fmaf(p, vv[c], acc[i][c]);
+      }
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < kValuRowsPerWave; ++i) {
+    const int R = rb * kValuRows + wave * kValuRowsPerWave + i;
+    if (R >= rows) continue;
+    const int n = R / a.group, head = hk * a.group + R % a.group;
+    const float inv = l_run[i] > 0.f ? 1.f / l_run[i] : 0.f;
+    const float lse2 = l_run[i] > 0.f ? m_run[i] + log2f(l_run[i]) : -INFINITY;
+    if (S == 1) {
+      const int64_t base = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+      for (int c = 0; c < D / 64; ++c) store_out(a, base + lane + 64 * c, acc[i][c] * inv);
+      if (lane == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] = lse2 * kLn2;
+    } else {
+      const int64_t pi = part_index(a, b, head, n, s);
+#pragma unroll
+      for (int c = 0; c < D / 64; ++c) a.part_o[pi * D + lane + 64 * c] = acc[i][c] * inv;
+      if (lane == 0) a.part_lse[pi] = lse2 * kLn2;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// MFMA split kernel (bf16 in, fp32 accumulate).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+union Pack8 {
+  uint4 u;
+  bf16x8 v;
+};
+
+// Position of token offset o (0..63) inside a transposed V row: within each
+// group of 16 tokens the two middle quads trade places, so that a lane's 8
+// consecutive positions hold the tokens the score MFMA left in that lane.
+CURE_DEV int v_pos(int o) {
+  const int qd = (o >> 2) & 3;
+  const int qs = (qd == 1) ? 2 : (qd == 2 ? 1 : qd);
+  return (o & ~15) | (qs << 2) | (o & 3);
+}
+
+// Transposed V rows are 64 tokens = eight 16-byte blocks; block index is
+// XOR-swizzled with bits of d to spread LDS banks for the quad writes.
+constexpr int kVStride = kTile + 8;   // bf16 elements per transposed V row
+CURE_DEV int v_addr(int d, int pos) {
+  const int blk = (pos >> 3) ^ ((d >> 3) & 7);
+  return d * kVStride + (blk << 3) + (pos & 7);
+}
+
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int kKStride = D + 8;                  // bf16 elements per K row in LDS
+  constexpr int kKChunks = kTile * D / 8;          // 16-byte chunks per K tile
+  constexpr int kKPer = (kKChunks + kThreads - 1) / kThreads;
+  constexpr int kVItems = (kTile / 4) * (D / 8);   // (quad of tokens, 8 columns)
+  constexpr int kVPer = (kVItems + kThreads - 1) / kThreads;
+  constexpr int kKSteps = D / 16;                  // MFMA k-steps for Q K^T
+  constexpr int kDBlk = D / 32;                    // 32-column blocks of O^T
+
+  __shared__ int s_parent[CURE_MAX_TREE_NODES];
+  __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
+  __shared__ int s_bad;
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[kTile * kKStride];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[D * kVStride];
+
+  const int b = blockIdx.z;
+  const int hk = blockIdx.y % a.hkv;
+  const int rb = blockIdx.y / a.hkv;
+  const int s = blockIdx.x;
+  const int N = min(a.n_nodes[b], a.n_max);
+  const int L = a.ctx_len[b];
+  const int T = L + N;
+  const int S = split_count(T, N, a.tps, a.max_splits);
+  const int rows = N * a.group;
+  if (s >= S || rb * a.rows_per_wg >= rows) return;
+  const bool reporter = s == 0 && hk == 0 && rb == 0;
+  const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
+  report_tree(a, b, ok, reporter);
+  if (!ok) return;
+
+  const int begin = s * a.tps;
+  const int end = (s == S - 1) ? T : begin + a.tps;
+  const int64_t off = a.kv_off[b];
+  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q);
+  const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k);
+  const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+
+  // This lane's query row.
+  const int R = rb * a.rows_per_wg + wave * 32 + col;
+  const bool row_ok = R < rows;
+  const int n = row_ok ? R / a.group : 0;
+  const int head = hk * a.group + (row_ok ? R % a.group : 0);
+  const bool wave_active = rb * a.rows_per_wg + wave * 32 < rows;
+
+  bf16x8 qreg[kKSteps];
+  {
+    const uint16_t* qrow = qp + (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+    for (int kk = 0; kk < kKSteps; ++kk) {
+      Pack8 p;
+      p.u = row_ok ? *reinterpret_cast<const uint4*>(qrow + kk * 16 + half * 8)
+                   : make_uint4(0, 0, 0, 0);
+      qreg[kk] = p.v;
+    }
+  }
+
+  f32x16 oacc[kDBlk];
+#pragma unroll
+  for (int i = 0; i < kDBlk; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  uint4 kreg[kKPer];
+  uint4 vreg[kVPer][4];
+  auto load_tile = [&](int t0) {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int c = tid + i * kThreads;
+      const int t = c / (D / 8), cc = (c % (D / 8)) * 8;
+      kreg[i] = make_uint4(0, 0, 0, 0);
+      if (c < kKChunks && t0 + t < end)
+        kreg[i] = *reinterpret_cast<const uint4*>(kp + ((off + t0 + t) * a.hkv + hk) * D + cc);
+    }
+#pragma unroll
+    for (int i = 0; i < kVPer; ++i) {
+      const int it = tid + i * kThreads;
+      const int g = it % (D / 8), qd = it / (D / 8);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = qd * 4 + j;
+        vreg[i][j] = make_uint4(0, 0, 0, 0);
+        if (it < kVItems && t0 + t < end)
+          vreg[i][j] = *reinterpret_cast<const uint4*>(vp + ((off + t0 + t) * a.hkv + hk) * D + g * 8);
+      }
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < kKPer; ++i) {
+      const int c = tid + i * kThreads;
+      if (c < kKChunks) {
+        const int t = c / (D / 8), cc = (c % (D / 8)) * 8;
+        *reinterpret_cast<uint4*>(&s_k[t * kKStride + cc]) = kreg[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kVPer; ++i) {
+      const int it = tid + i * kThreads;
+      if (it < kVItems) {
+        const int g = it % (D / 8), qd = it / (D / 8);
+        const int pos = v_pos(qd * 4);
+        const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
+        const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+        const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
+        const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int sh = (e & 1) * 16;
+          const uint32_t x0 = (w0[e >> 1] >> sh) & 0xffffu, x1 = (w1[e >> 1] >> sh) & 0xffffu;
+          const uint32_t x2 = (w2[e >> 1] >> sh) & 0xffffu, x3 = (w3[e >> 1] >> sh) & 0xffffu;
+          uint2 pk;
+          pk.x = x0 | (x1 << 16);
+          pk.y = x2 | (x3 << 16);
+          *reinterpret_cast<uint2*>(&s_v[v_addr(g * 8 + e, pos)]) = pk;
+        }
+      }
+    }
+  };
+
+  load_tile(begin);
+  for (int t0 = begin; t0 < end; t0 += kTile) {
+    __syncthreads();                      // previous tile fully consumed
+    store_tile();
+    __syncthreads();
+    if (t0 + kTile < end) load_tile(t0 + kTile);
+    if (!wave_active) continue;
+
+    // S^T (tokens x query rows) for two 32-token blocks.
+    // The two token blocks are independent accumulation chains; interleaving
+    // them keeps two MFMAs in flight.
+    f32x16 sacc[2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[blk][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < kKSteps; ++kk) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        Pack8 ka;
+        ka.u = *reinterpret_cast<const uint4*>(&s_k[(blk * 32 + col) * kKStride + kk * 16 + half * 8]);
+        sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka.v, qreg[kk], sacc[blk], 0, 0, 0);
+      }
+    }
+    // Scale into the log2 domain and mask the tail.
+    const bool masked = t0 + kTile > L;
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x = sacc[blk][r] * a.scale_log2;
+        if (masked) {
+          const int tok = t0 + blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (!(tok < end && visible(tok, L, N, n, s_anc))) x = -INFINITY;
+        }
+        sacc[blk][r] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    const float m_tile = fmaxf(mloc, shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_run, m_tile);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run - m_use);
+    float psum = 0.f;
+    bf16x8 pb[4];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        bf16x8 v8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = fast_exp2(sacc[blk][8 * j + e] - m_use);
+          psum += p;
+          v8[e] = (__bf16)p;
+        }
+        pb[blk * 2 + j] = v8;
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int i = 0; i < kDBlk; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+
+    // O^T += V^T P^T; the D/32 column blocks are independent chains, interleaved.
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int i = 0; i < kDBlk; ++i) {
+        Pack8 va;
+        va.u = *reinterpret_cast<const uint4*>(&s_v[v_addr(i * 32 + col, ks * 16 + half * 8)]);
+        oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va.v, pb[ks], oacc[i], 0, 0, 0);
+      }
+    }
+  }
+
+  if (!row_ok) return;
+  const float l_tot = l_run + shfl_xor(l_run, 32);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse_nat = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+  if (S == 1) {
+    const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+    for (int i = 0; i < kDBlk; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = i * 32 + 8 * g4 + 4 * half;
+        const float x0 = oacc[i][4 * g4] * inv, x1 = oacc[i][4 * g4 + 1] * inv;
+        const float x2 = oacc[i][4 * g4 + 2] * inv, x3 = oacc[i][4 * g4 + 3] * inv;
+        if (a.out_bf16) {
+          uint2 pk;
+          pk.x = pack_bf16x2(x0, x1);
+          pk.y = pack_bf16x2(x2, x3);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.o) + obase + d0) = pk;
+        } else {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.o) + obase + d0) =
+              make_float4(x0, x1, x2, x3);
+        }
+      }
+    if (half == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] = lse_nat;
+  } else {
+    const int64_t pi = part_index(a, b, head, n, s);
+#pragma unroll
+    for (int i = 0; i < kDBlk; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = i * 32 + 8 * g4 + 4 * half;
+        *reinterpret_cast<float4*>(a.part_o + pi * D + d0) =
+            make_float4(oacc[i][4 * g4] * inv, oacc[i][4 * g4 + 1] * inv,
+                        oacc[i][4 * g4 + 2] * inv, oacc[i][4 * g4 + 3] * inv);
+      }
+    if (half == 0) a.part_lse[pi] = lse_nat;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LSE merge: one wave per output row (b, n, head).
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t nrows = (int64_t)batch * a.n_max * a.hq;
+  if (rowid >= nrows) return;
+  const int head = (int)(rowid % a.hq);
+  const int n = (int)((rowid / a.hq) % a.n_max);
+  const int b = (int)(rowid / ((int64_t)a.hq * a.n_max));
+  const int N = min(a.n_nodes[b], a.n_max);
+  if (n >= N) return;
+  const int S = split_count(a.ctx_len[b] + N, N, a.tps, a.max_splits);
+  if (S <= 1) return;
+  const int64_t p0 = part_index(a, b, head, n, 0);
+  float m = -INFINITY;
+  for (int s = lane; s < S; s += 64) m = fmaxf(m, a.part_lse[p0 + s]);
+#pragma unroll
+  for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor(m, k));
+  float acc[D / 64] = {};
+  float wsum = 0.f;
+  if (m != -INFINITY) {
+    for (int s = 0; s < S; ++s) {
+      const float w = __expf(a.part_lse[p0 + s] - m);
+      wsum += w;
+#pragma unroll
+      for (int c = 0; c < D / 64; ++c) acc[c] = fmaf(w, a.part_o[(p0 + s) * D + lane + 64 * c], acc[c]);
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+  for (int c = 0; c < D / 64; ++c) store_out(a, obase + lane + 64 * c, acc[c] * inv);
+  if (lane == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] =
+      wsum > 0.f ? m + logf(wsum) : -INFINITY;
+}
+
+// ---------------------------------------------------------------------------
+// Host-side plan: tokens per split and the launch shape.
+struct Plan {
+  bool mfma;
+  int nw;             // waves per workgroup (MFMA kernel)
+  int rows_per_wg;
+  int row_blocks;
+  int tps;
+  int max_splits;
+};
+
+Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
+               const int32_t* host_ctx_len, const int32_t* host_n_nodes, int32_t kv_split,
+               bool mfma) {
+  Plan p{};
+  p.mfma = mfma;
+  const int group = hq / hkv;
+  const int rows = n_max * group;
+  if (mfma) {
+    p.nw = rows <= 128 ? 4 : 8;
+    p.rows_per_wg = 32 * p.nw;
+  } else {
+    p.nw = kValuWaves;
+    p.rows_per_wg = kValuRows;
+  }
+  p.row_blocks = std::max(1, (rows + p.rows_per_wg - 1) / p.rows_per_wg);
+  int64_t t_max = 0, t_sum = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int N = std::min(host_n_nodes[b], n_max);
+    if (N <= 0) continue;
+    const int64_t T = (int64_t)host_ctx_len[b] + N;
+    t_max = std::max(t_max, T);
+    t_sum += T;
+  }
+  int64_t tps;
+  if (kv_split > 0) {
+    tps = (t_max + kv_split - 1) / kv_split;
+  } else {
+    const int64_t target = 2LL * device_cu_count();
+    const int64_t work = t_sum * hkv * p.row_blocks;
+    tps = std::max<int64_t>(kMinTps, (work + target - 1) / std::max<int64_t>(1, target));
+  }
+  tps = std::max<int64_t>(kTile, (tps + kTile - 1) / kTile * kTile);
+  p.tps = (int)std::min<int64_t>(tps, INT32_MAX / 2);
+  p.max_splits = t_max > 0 ? (int)((t_max + p.tps - 1) / p.tps) : 0;
+  return p;
+}
+
+size_t plan_workspace(const Plan& p, int32_t batch, int32_t hq, int32_t d, int32_t n_max) {
+  if (p.max_splits <= 1) return 0;
+  const size_t parts = (size_t)batch * hq * n_max * p.max_splits;
+  return align_up(parts * d * sizeof(float), 256) + align_up(parts * sizeof(float), 256);
+}
+
+bool use_mfma(int32_t dtype, int32_t d, uint32_t flags) {
+  return dtype == CURE_BF16 && (d == 64 || d == 128) && !(flags & CURE_ATTN_FORCE_VALU);
+}
+
+}  // namespace
+}  // namespace cure
+
+using namespace cure;
+
+extern "C" size_t cure_tree_attn_workspace_size(int32_t batch, int32_t hq, int32_t hkv,
+                                                int32_t d, int32_t n_max,
+                                                const int32_t* host_ctx_len,
+                                                const int32_t* host_n_nodes,
+                                                int32_t kv_split) {
+  if (batch <= 0 || hq <= 0 || hkv <= 0 || hq % hkv || n_max <= 0 || !host_ctx_len ||
+      !host_n_nodes)
+    return 0;
+  // The MFMA and VALU plans may differ in row blocking; report the larger need.
+  const Plan pm = make_plan(batch, hq, hkv, d, n_max, host_ctx_len, host_n_nodes, kv_split, true);
+  const Plan pv = make_plan(batch, hq, hkv, d, n_max, host_ctx_len, host_n_nodes, kv_split, false);
+  return std::max(plan_workspace(pm, batch, hq, d, n_max), plan_workspace(pv, batch, hq, d, n_max));
+}
+
+extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* v, void* o,
+                                      float* lse, int32_t dtype, int32_t out_dtype,
+                                      int32_t batch, int32_t hq, int32_t hkv, int32_t d,
+                                      float scale, const int64_t* kv_off,
+                                      const int32_t* ctx_len, const int32_t* n_nodes,
+                                      const int32_t* parent, int32_t n_max,
+                                      const int32_t* host_ctx_len,
+                                      const int32_t* host_n_nodes, int32_t kv_split,
+                                      uint32_t flags, int32_t* tree_status, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  if (dtype != CURE_F32 && dtype != CURE_BF16) return CURE_ERR_INVALID_ARG;
+  if (out_dtype != CURE_F32 && out_dtype != CURE_BF16) return CURE_ERR_INVALID_ARG;
+  if (batch < 0 || hq <= 0 || hkv <= 0 || n_max < 0 || kv_split < 0) return CURE_ERR_INVALID_ARG;
+  if (hq % hkv != 0) return CURE_ERR_INVALID_ARG;
+  if (d != 64 && d != 128) return CURE_ERR_UNSUPPORTED;
+  if (n_max > CURE_MAX_TREE_NODES) return CURE_ERR_UNSUPPORTED;
+  if (batch == 0 || n_max == 0) return CURE_OK;
+  if (!q || !k || !v || !o || !kv_off || !ctx_len || !n_nodes || !parent || !host_ctx_len ||
+      !host_n_nodes)
+    return CURE_ERR_INVALID_ARG;
+  for (int b = 0; b < batch; ++b)
+    if (host_ctx_len[b] < 0 || host_n_nodes[b] < 0 || host_n_nodes[b] > n_max)
+      return CURE_ERR_INVALID_ARG;
+  const bool mfma = use_mfma(dtype, d, flags);
+  const Plan p = make_plan(batch, hq, hkv, d, n_max, host_ctx_len, host_n_nodes, kv_split, mfma);
+  if (p.max_splits == 0) return CURE_OK;    // no sequence has tree nodes
+  const size_t need = plan_workspace(p, batch, hq, d, n_max);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return CURE_ERR_WORKSPACE;
+  if ((size_t)p.row_blocks * hkv > 65535 || batch > 65535) return CURE_ERR_UNSUPPORTED;
+
+  Args a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.lse = lse;
+  a.out_bf16 = out_dtype == CURE_BF16;
+  a.hq = hq;
+  a.hkv = hkv;
+  a.group = hq / hkv;
+  a.n_max = n_max;
+  a.scale_log2 = scale * kLog2e;
+  a.kv_off = kv_off;
+  a.ctx_len = ctx_len;
+  a.n_nodes = n_nodes;
+  a.parent = parent;
+  a.tps = p.tps;
+  a.max_splits = p.max_splits;
+  a.rows_per_wg = p.rows_per_wg;
+  a.tree_status = tree_status;
+  if (need > 0) {
+    const size_t parts = (size_t)batch * hq * n_max * p.max_splits;
+    a.part_o = reinterpret_cast<float*>(workspace);
+    a.part_lse = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                          align_up(parts * d * sizeof(float), 256));
+  }
+  if (mfma) {
+    // The MFMA kernel reads q, k and v as 16-byte vectors.
+    const uintptr_t mis = reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(k) |
+                          reinterpret_cast<uintptr_t>(v);
+    if (mis % 16 != 0) return CURE_ERR_INVALID_ARG;
+    if (a.out_bf16 ? reinterpret_cast<uintptr_t>(o) % 8 : reinterpret_cast<uintptr_t>(o) % 16)
+      return CURE_ERR_INVALID_ARG;
+  }
+
+  hipStream_t st = as_stream(stream);
+  const dim3 grid(p.max_splits, hkv * p.row_blocks, batch);
+  if (mfma) {
+    if (d == 128) {
+      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<128, 4>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_mfma<128, 8>), grid, dim3(512), 0, st, a);
+    } else {
+      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<64, 4>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_mfma<64, 8>), grid, dim3(512), 0, st, a);
+    }
+  } else {
+    if (dtype == CURE_BF16) {
+      if (d == 128) hipLaunchKernelGGL((tree_attn_valu<uint16_t, 128>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_valu<uint16_t, 64>), grid, dim3(256), 0, st, a);
+    } else {
+      if (d == 128) hipLaunchKernelGGL((tree_attn_valu<float, 128>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_valu<float, 64>), grid, dim3(256), 0, st, a);
+    }
+  }
+  if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
+  if (p.max_splits > 1) {
+    const int64_t nrows = (int64_t)batch * n_max * hq;
+    const dim3 mgrid((unsigned)((nrows + 3) / 4));
+    if (d == 128) hipLaunchKernelGGL((attn_merge<128>), mgrid, dim3(256), 0, st, a, batch);
+    else hipLaunchKernelGGL((attn_merge<64>), mgrid, dim3(256), 0, st, a, batch);
+  }
+  return launch_status();
+}

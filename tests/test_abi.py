@@ -1,0 +1,137 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/cure.h, and rejects bad arguments before touching a device.
+
+Calls here pass fake device pointers, so every call is built to stop at a
+host-side argument check: none may reach a kernel launch (these tests must be
+safe on a GPU machine too).
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_00531_amd as pc
+from paper_2608_00531_amd import build as pbuild
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "cure.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(pbuild.LIB_PATH):
+        pbuild.build_library()
+    return pc.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cure_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_entry_points():
+    names = declared_functions()
+    for fn in ("cure_margins", "cure_tree_attn", "cure_accept"):
+        assert fn in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_status_strings_and_version(L):
+    assert L.cure_status_string(0) == b"CURE_OK"
+    assert L.cure_status_string(3) == b"CURE_ERR_BAD_TREE"
+    assert L.cure_status_string(99) == b"CURE_ERR_UNKNOWN"
+    assert L.cure_version() >= 100
+
+
+def _margins(L, **kw):
+    # vocab 100000 over 4 rows always plans several chunks per row, so a
+    # missing workspace is reported before any launch.
+    args = dict(logits=1, dtype=1, batch=1, rows=4, vocab=100000, ld=100000,
+                top1_val=1, top1_idx=1, top2_val=1, top2_idx=1, lse=1, margin=1,
+                chain_len=2, tau=1.0, repair_budget=4, branch_depth=2, ufp_pos=1, ufp_cnt=1,
+                workspace=None, ws_bytes=0, stream=None)
+    args.update(kw)
+    return L.cure_margins(*args.values())
+
+
+def test_margins_argument_errors(L):
+    assert _margins(L, dtype=7) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, vocab=1, ld=1) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, ld=50000) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, logits=None) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, margin=None) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, chain_len=5) == pc.CURE_ERR_INVALID_ARG        # > rows
+    assert _margins(L, branch_depth=0) == pc.CURE_ERR_INVALID_ARG
+    assert _margins(L, ufp_cnt=None) == pc.CURE_ERR_INVALID_ARG      # half a gate
+    assert _margins(L, rows=2000, chain_len=1500) == pc.CURE_ERR_UNSUPPORTED
+    assert _margins(L) == pc.CURE_ERR_WORKSPACE                        # no workspace
+    assert _margins(L, batch=0) == pc.CURE_OK                          # empty: nothing to do
+    assert _margins(L, batch=-1) == pc.CURE_ERR_INVALID_ARG
+
+
+def test_margins_workspace_size_grows_with_rows(L):
+    a = L.cure_margins_workspace_size(1, 32, 128256)
+    b = L.cure_margins_workspace_size(16, 48, 128256)
+    assert a > 0 and b > a and b % 256 == 0
+
+
+def _attn(L, **kw):
+    ctx = np.array([10], np.int32)
+    nn = np.array([3], np.int32)
+    args = dict(q=1, k=1, v=1, o=1, lse=None, dtype=1, out_dtype=1, batch=1, hq=4, hkv=2,
+                d=64, scale=0.125, kv_off=1, ctx_len=1, n_nodes=1, parent=1, n_max=3,
+                host_ctx_len=ctx.ctypes.data_as(ctypes.c_void_p),
+                host_n_nodes=nn.ctypes.data_as(ctypes.c_void_p), kv_split=0, flags=0,
+                tree_status=None, workspace=None, ws_bytes=0, stream=None)
+    args.update(kw)
+    return L.cure_tree_attn(*args.values())
+
+
+def test_tree_attn_argument_errors(L):
+    assert _attn(L, d=96) == pc.CURE_ERR_UNSUPPORTED
+    assert _attn(L, n_max=300) == pc.CURE_ERR_UNSUPPORTED
+    assert _attn(L, hq=5) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, dtype=3) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, q=None) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, parent=None) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, host_ctx_len=None) == pc.CURE_ERR_INVALID_ARG
+    bad_n = np.array([4], np.int32)                                    # more nodes than n_max
+    assert _attn(L, host_n_nodes=bad_n.ctypes.data_as(ctypes.c_void_p)) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, batch=0) == pc.CURE_OK
+
+
+def test_tree_attn_workspace_size_tracks_splits(L):
+    ctx = np.array([32768] * 4, np.int32)
+    nn = np.array([32] * 4, np.int32)
+    cp, np_ = ctx.ctypes.data_as(ctypes.c_void_p), nn.ctypes.data_as(ctypes.c_void_p)
+    one = L.cure_tree_attn_workspace_size(4, 32, 8, 128, 32, cp, np_, 1)
+    eight = L.cure_tree_attn_workspace_size(4, 32, 8, 128, 32, cp, np_, 8)
+    assert one == 0                                      # a single split needs no partials
+    assert eight >= 4 * 32 * 32 * 8 * 129 * 4
+
+
+def test_accept_argument_errors(L):
+    args = [1, 1, 1, 1, 1, 4, 2, 8, 1, 1, 1, 1, 1, None]
+    bad = list(args)
+    bad[7] = 300                                                       # n_max > 256
+    assert L.cure_accept(*bad) == pc.CURE_ERR_UNSUPPORTED
+    bad = list(args)
+    bad[0] = None
+    assert L.cure_accept(*bad) == pc.CURE_ERR_INVALID_ARG
+    bad = list(args)
+    bad[6] = 0
+    assert L.cure_accept(*bad) == pc.CURE_OK                           # empty batch
+
+
+def test_binding_fails_loudly_without_gpu_tensors():
+    import torch
+    with pytest.raises(pc.CureError):
+        pc.cure_margins(torch.zeros(2, 16))

@@ -1,0 +1,71 @@
+"""GPU: the whole verify-and-repair step (margins -> tree attention -> accept)
+on named workloads, chained exactly as the benchmark chains it, checked against
+the oracle chained the same way; and the step captured as a HIP graph,
+replayed several times with eager work in between, each replay checked
+against the eager result.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_00531_amd as pc
+from synth import preset
+from parity_util import (say, upload, gpu_margins, gpu_attn, check_margins, check_attn,
+                         check_accept, oracle_attn)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_step(w, dev):
+    m = gpu_margins(w, dev)
+    o, lse, st = gpu_attn(w, dev)
+    acc = pc.cure_accept(dev["parent"], dev["token"], m["top1_idx"], dev["root_tgt"],
+                         dev["n_nodes"], w.chain_len)
+    return m, (o, lse, st), acc
+
+
+@pytest.mark.parametrize("name", ["tiny_fp32", "llama3_8b_ctx2k_b1",
+                                  "llama3_8b_ctx8k_b8_budget32"])
+def test_step_chain_matches_oracle_chain(name):
+    say("step", name)
+    w = preset(name)
+    dev = upload(w)
+    m, (o, lse, st), acc = run_step(w, dev)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK] * w.batch
+    check_margins(w, m)
+    tgt = np.stack([oracle.margins(w.logits[b], w.dtype)["top1_idx"] for b in range(w.batch)])
+    assert np.array_equal(tgt, w.tgt_planted)
+    check_accept(w, acc, tgt)
+    sample = [(b, n) for b in range(w.batch) for n in (0, int(w.n_nodes[b]) - 1)]
+    ref_o, ref_l = oracle_attn(w, sample=sample)
+    check_attn(w, o, lse, ref_o, ref_l, sample=sample)
+
+
+def test_graph_replays_match_eager():
+    say("step graph replay")
+    w = preset("llama3_8b_ctx2k_b1")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dev = upload(w)
+        eager = run_step(w, dev)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            cap = run_step(w, dev)
+        for rep in range(4):
+            # Eager work and a synchronisation between replays.
+            junk = torch.randn(1 << 20, device="cuda").sum()
+            torch.cuda.synchronize()
+            for t in (cap[0]["top1_idx"], cap[2]["acc_len"], cap[1][0]):
+                t.fill_(-7) if t.dtype != torch.bfloat16 else t.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            for key in ("top1_idx", "top2_idx", "margin", "lse", "ufp_pos", "ufp_cnt"):
+                assert torch.equal(cap[0][key], eager[0][key]), (rep, key)
+            assert torch.equal(cap[1][0], eager[1][0]) and torch.equal(cap[1][1], eager[1][1])
+            for key in ("acc_len", "path", "best", "bonus", "resync"):
+                assert torch.equal(cap[2][key], eager[2][key]), (rep, key)
+            del junk
