@@ -60,10 +60,12 @@ struct Args {
   Partial* partials;     // [rows total][splits], only when splits > 1
 };
 
-// Raw buffer loads: the chunk is described by a buffer resource (base, size),
-// lane offsets are 32-bit and the per-step offset is a scalar, so the loop
-// carries no 64-bit address arithmetic. Reads at or past the resource's size
-// return zero instead of touching memory.
+// Raw buffer loads: the chunk is described by a buffer resource (base, size)
+// and every load carries a 32-bit per-lane offset, so the loop carries no
+// 64-bit address arithmetic. The hardware range-checks the per-lane (VGPR)
+// offset against the resource size -- the scalar offset operand is not
+// checked, so it is always 0 here -- and reads at or past the size return zero
+// without touching memory.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kRsrcWord3 = 0x00020000;   // raw (untyped) 32-bit access, gfx9 family
 
@@ -77,8 +79,8 @@ struct Raw8;
 template <>
 struct Raw8<uint16_t> {
   u32x4 w;
-  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t step_off) {
-    w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)step_off, 0);
+  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
   }
   static constexpr uint32_t kBytes = 16;
   CURE_DEV void widen(float (&f)[kVec]) const {
@@ -91,9 +93,9 @@ struct Raw8<uint16_t> {
 template <>
 struct Raw8<float> {
   u32x4 a, b;
-  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t step_off) {
-    a = __builtin_amdgcn_raw_buffer_load_b128(r, (int)lane_off, (int)step_off, 0);
-    b = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(lane_off + 16), (int)step_off, 0);
+  CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    a = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    b = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(off + 16), 0, 0);
   }
   static constexpr uint32_t kBytes = 32;
   CURE_DEV void widen(float (&f)[kVec]) const {
@@ -195,7 +197,7 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
       auto issue = [&](Raw8<T>(&r)[kUnroll], int it) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-          r[u].load(rsrc, lane_off, (uint32_t)((it * kUnroll + u) * kThreads) * Raw8<T>::kBytes);
+          r[u].load(rsrc, lane_off + (uint32_t)((it * kUnroll + u) * kThreads) * Raw8<T>::kBytes);
       };
       auto process = [&](const Raw8<T>(&r)[kUnroll], int it) {
 #pragma unroll

@@ -11,19 +11,22 @@
 // at the tail of the sequence apply the ancestor bitmask.
 //
 // Two kernels compute a split:
-//  * tree_attn_mfma: bf16, head dim 64/128. Scores are formed transposed,
-//    S^T = K Q^T, and the output as O^T = V^T P^T with 32x32x16 bf16 MFMAs, so
-//    each lane owns one query row and the online softmax needs no cross-lane
-//    traffic beyond one swap between the two half-waves. V is staged in LDS
-//    transposed (token-minor) with the token order inside each 16-token group
-//    permuted to match where the score MFMA leaves P in registers.
-//  * tree_attn_valu: fp32 or bf16, any supported shape; plain vector ALU code.
+//  * tree_attn_mfma: bf16, head dim 64/128, scale > 0. Scores are formed
+//    transposed, S^T = K Q^T, and the output as O^T = V^T P^T with 32x32x16
+//    bf16 MFMAs, so each lane owns one query row and the online softmax needs
+//    no cross-lane traffic beyond one exchange between the two half-waves.
+//    K/V tiles arrive in LDS by DMA; V is read back transposed by the LDS
+//    transpose-read instruction in exactly the token order the score MFMA
+//    leaves P in registers.
+//  * tree_attn_valu: fp32 or bf16, any supported shape and scale; plain vector
+//    ALU code.
 // A split writes normalised partial O and its log-sum-exp; attn_merge combines
 // the splits of each row (skipped when a sequence has a single split, in which
 // case the split kernel writes the final output itself).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <vector>
 
 #include "common.hpp"
@@ -259,47 +262,65 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
 
 // ---------------------------------------------------------------------------
 // MFMA split kernel (bf16 in, fp32 accumulate).
+//
+// Each of the NW waves owns 32 query rows. Per 64-token tile:
+//   S^T = K Q^T  (2 token blocks x D/16 k-steps of 32x32x16 MFMA; lane = query row)
+//   online softmax in the log2 domain, rescaling O only when a row's maximum
+//   rises by more than 2^8 (values then stay below 2^8, safe in bf16 and fp32)
+//   O^T += V^T P^T (D/32 column blocks x 4 k-steps)
+// K and V tiles move HBM -> LDS by DMA (buffer loads that write LDS directly),
+// double-buffered so the next tile streams in while this one is computed. The
+// per-sequence buffer resource bounds every read: rows past the sequence end
+// read as zeros. LDS rows are 16-byte-chunk XOR-swizzled so that both the K
+// reads (one row per lane) and the transposed V reads (4 rows x 16 columns per
+// 16 lanes, ds_read_b64_tr_b16) spread over the banks.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 union Pack8 {
   uint4 u;
   bf16x8 v;
+  i16x4 h[2];
 };
 
-// Position of token offset o (0..63) inside a transposed V row: within each
-// group of 16 tokens the two middle quads trade places, so that a lane's 8
-// consecutive positions hold the tokens the score MFMA left in that lane.
-CURE_DEV int v_pos(int o) {
-  const int qd = (o >> 2) & 3;
-  const int qs = (qd == 1) ? 2 : (qd == 2 ? 1 : qd);
-  return (o & ~15) | (qs << 2) | (o & 3);
-}
+constexpr int kRsrcWord3 = 0x00020000;     // raw (untyped) 32-bit access, gfx9 family
+constexpr float kRescaleLog2 = 8.f;       // lazy rescale threshold (log2 units)
 
-// Transposed V rows are 64 tokens = eight 16-byte blocks; block index is
-// XOR-swizzled with bits of d to spread LDS banks for the quad writes.
-constexpr int kVStride = kTile + 8;   // bf16 elements per transposed V row
-CURE_DEV int v_addr(int d, int pos) {
-  const int blk = (pos >> 3) ^ ((d >> 3) & 7);
-  return d * kVStride + (blk << 3) + (pos & 7);
-}
+template <int D>
+struct TileGeo {
+  static constexpr int kChunks = D / 8;             // 16-byte chunks per row
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kTileBytes = kTile * kRowBytes;
+  static constexpr int kBlocks = kTileBytes / 1024;  // 1 KB DMA blocks per tile
+  // Swizzle: the chunk index is XORed with a row-dependent value so that 16
+  // consecutive rows use 16 different chunk slots, and 4 consecutive rows
+  // (starting at a multiple of 4) keep their chunk pairs aligned.
+  static CURE_DEV int swz(int row) {
+    constexpr int h = kChunks / 2;
+    return ((row & (h - 1)) << 1) | ((row / h) & 1);
+  }
+  static CURE_DEV int offset(int row, int chunk) {   // byte offset inside a tile
+    return row * kRowBytes + ((chunk ^ swz(row)) << 4);
+  }
+};
 
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
-  constexpr int kThreads = 64 * NW;
-  constexpr int kKStride = D + 8;                  // bf16 elements per K row in LDS
-  constexpr int kKChunks = kTile * D / 8;          // 16-byte chunks per K tile
-  constexpr int kKPer = (kKChunks + kThreads - 1) / kThreads;
-  constexpr int kVItems = (kTile / 4) * (D / 8);   // (quad of tokens, 8 columns)
-  constexpr int kVPer = (kVItems + kThreads - 1) / kThreads;
+__global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
+  using G = TileGeo<D>;
   constexpr int kKSteps = D / 16;                  // MFMA k-steps for Q K^T
   constexpr int kDBlk = D / 32;                    // 32-column blocks of O^T
+  constexpr int kDmaPerWave = G::kBlocks / NW;     // DMA blocks per wave per tensor
+  static_assert(G::kBlocks % NW == 0, "tile must split evenly across waves");
 
   __shared__ int s_parent[CURE_MAX_TREE_NODES];
   __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
   __shared__ int s_bad;
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[kTile * kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[D * kVStride];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_k[2][G::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_v[2][G::kTileBytes];
 
   const int b = blockIdx.z;
   const int hk = blockIdx.y % a.hkv;
@@ -319,11 +340,37 @@ __global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
   const int begin = s * a.tps;
   const int end = (s == S - 1) ? T : begin + a.tps;
   const int64_t off = a.kv_off[b];
-  const uint16_t* qp = reinterpret_cast<const uint16_t*>(a.q);
-  const uint16_t* kp = reinterpret_cast<const uint16_t*>(a.k);
-  const uint16_t* vp = reinterpret_cast<const uint16_t*>(a.v);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
+
+  // Buffer resources over this sequence's K and V rows (all kv-heads).
+  const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.k)) + off * a.hkv * D, 0,
+      (int)seq_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.v)) + off * a.hkv * D, 0,
+      (int)seq_bytes, kRsrcWord3);
+  // Per lane and DMA block: byte offset of the source chunk for tile start 0.
+  uint32_t src_off[kDmaPerWave];
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int byte = (wave * kDmaPerWave + j) * 1024 + lane * 16;   // destination in tile
+    const int row = byte / G::kRowBytes;
+    const int pchunk = (byte % G::kRowBytes) >> 4;
+    const int lchunk = pchunk ^ G::swz(row);
+    src_off[j] = (uint32_t)((row * a.hkv + hk) * G::kRowBytes + (lchunk << 4));
+  }
+  const uint32_t tok_bytes = (uint32_t)(a.hkv * G::kRowBytes);
+  auto dma_tile = [&](int buf, int t0) {
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) {
+      const uint32_t voff = src_off[j] + (uint32_t)t0 * tok_bytes;
+      const int blk = (wave * kDmaPerWave + j) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(&s_k[buf][blk]), 16, (int)voff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(&s_v[buf][blk]), 16, (int)voff, 0, 0, 0);
+    }
+  };
 
   // This lane's query row.
   const int R = rb * a.rows_per_wg + wave * 32 + col;
@@ -334,7 +381,8 @@ __global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
 
   bf16x8 qreg[kKSteps];
   {
-    const uint16_t* qrow = qp + (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                           (((int64_t)b * a.n_max + n) * a.hq + head) * D;
 #pragma unroll
     for (int kk = 0; kk < kKSteps; ++kk) {
       Pack8 p;
@@ -344,81 +392,42 @@ __global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
     }
   }
 
+  // LDS byte offsets used by this lane, independent of the tile.
+  // K rows blk*32 + col, logical chunk 2*kk + half.
+  int k_row_base[2], k_swz[2];
+#pragma unroll
+  for (int blk = 0; blk < 2; ++blk) {
+    const int row = blk * 32 + col;
+    k_row_base[blk] = row * G::kRowBytes;
+    k_swz[blk] = G::swz(row) ^ half;
+  }
+  // V transposed reads: lane j of each 16-lane group reads 8 bytes at row
+  // (4*half + j/4) of a 4-row group, columns 4*(j%4) of a 16-column block.
+  const int j16 = lane & 15, g16 = (lane >> 4) & 1;
+  const int v_row_lane = 4 * half + (j16 >> 2);          // + 16*ks + 8*r
+  const int v_chunk_lane = 2 * g16 + ((j16 & 3) >> 1);   // + 4*i
+  const int v_byte_lane = (j16 & 1) * 8;
+
   f32x16 oacc[kDBlk];
 #pragma unroll
   for (int i = 0; i < kDBlk; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  const float c = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  uint4 kreg[kKPer];
-  uint4 vreg[kVPer][4];
-  auto load_tile = [&](int t0) {
-#pragma unroll
-    for (int i = 0; i < kKPer; ++i) {
-      const int c = tid + i * kThreads;
-      const int t = c / (D / 8), cc = (c % (D / 8)) * 8;
-      kreg[i] = make_uint4(0, 0, 0, 0);
-      if (c < kKChunks && t0 + t < end)
-        kreg[i] = *reinterpret_cast<const uint4*>(kp + ((off + t0 + t) * a.hkv + hk) * D + cc);
-    }
-#pragma unroll
-    for (int i = 0; i < kVPer; ++i) {
-      const int it = tid + i * kThreads;
-      const int g = it % (D / 8), qd = it / (D / 8);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int t = qd * 4 + j;
-        vreg[i][j] = make_uint4(0, 0, 0, 0);
-        if (it < kVItems && t0 + t < end)
-          vreg[i][j] = *reinterpret_cast<const uint4*>(vp + ((off + t0 + t) * a.hkv + hk) * D + g * 8);
-      }
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < kKPer; ++i) {
-      const int c = tid + i * kThreads;
-      if (c < kKChunks) {
-        const int t = c / (D / 8), cc = (c % (D / 8)) * 8;
-        *reinterpret_cast<uint4*>(&s_k[t * kKStride + cc]) = kreg[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kVPer; ++i) {
-      const int it = tid + i * kThreads;
-      if (it < kVItems) {
-        const int g = it % (D / 8), qd = it / (D / 8);
-        const int pos = v_pos(qd * 4);
-        const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-        const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
-        const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
-        const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int sh = (e & 1) * 16;
-          const uint32_t x0 = (w0[e >> 1] >> sh) & 0xffffu, x1 = (w1[e >> 1] >> sh) & 0xffffu;
-          const uint32_t x2 = (w2[e >> 1] >> sh) & 0xffffu, x3 = (w3[e >> 1] >> sh) & 0xffffu;
-          uint2 pk;
-          pk.x = x0 | (x1 << 16);
-          pk.y = x2 | (x3 << 16);
-          *reinterpret_cast<uint2*>(&s_v[v_addr(g * 8 + e, pos)]) = pk;
-        }
-      }
-    }
-  };
-
-  load_tile(begin);
-  for (int t0 = begin; t0 < end; t0 += kTile) {
-    __syncthreads();                      // previous tile fully consumed
-    store_tile();
-    __syncthreads();
-    if (t0 + kTile < end) load_tile(t0 + kTile);
+  dma_tile(0, begin);
+  int buf = 0;
+  for (int t0 = begin; t0 < end; t0 += kTile, buf ^= 1) {
+    __builtin_amdgcn_s_waitcnt(0);        // this wave's DMA into `buf` has landed
+    __syncthreads();                      // everyone's has; `buf ^ 1` is free again
+    if (t0 + kTile < end) dma_tile(buf ^ 1, t0 + kTile);
     if (!wave_active) continue;
+    const unsigned char* kt = s_k[buf];
+    const unsigned char* vt = s_v[buf];
 
-    // S^T (tokens x query rows) for two 32-token blocks.
-    // The two token blocks are independent accumulation chains; interleaving
-    // them keeps two MFMAs in flight.
+    // S^T (tokens x query rows), raw dot products; two independent chains.
     f32x16 sacc[2];
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
@@ -429,58 +438,71 @@ __global__ __launch_bounds__(64 * NW) void tree_attn_mfma(Args a) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
         Pack8 ka;
-        ka.u = *reinterpret_cast<const uint4*>(&s_k[(blk * 32 + col) * kKStride + kk * 16 + half * 8]);
+        ka.u = *reinterpret_cast<const uint4*>(kt + k_row_base[blk] + (((2 * kk) ^ k_swz[blk]) << 4));
         sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka.v, qreg[kk], sacc[blk], 0, 0, 0);
       }
     }
-    // Scale into the log2 domain and mask the tail.
-    const bool masked = t0 + kTile > L;
+    // Mask the tail, then the tile's row maximum (raw units; the scale is > 0).
+    if (t0 + kTile > L) {
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int tok = t0 + blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          if (!(tok < end && visible(tok, L, N, n, s_anc))) sacc[blk][r] = -INFINITY;
+        }
+    }
     float mloc = -INFINITY;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = sacc[blk][r] * a.scale_log2;
-        if (masked) {
-          const int tok = t0 + blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (!(tok < end && visible(tok, L, N, n, s_anc))) x = -INFINITY;
-        }
-        sacc[blk][r] = x;
-        mloc = fmaxf(mloc, x);
+      for (int r = 0; r < 16; r += 2) mloc = fmaxf(mloc, fmaxf(sacc[blk][r], sacc[blk][r + 1]));
+    const float m_tile = fmaxf(mloc, shfl_xor(mloc, 32)) * c;
+    // Lazy rescale: move the reference only when the maximum rises by > 2^8.
+    const bool grow = m_tile > m_run + kRescaleLog2;
+    if (__builtin_expect(__ballot(grow) != 0, 0)) {
+      if (grow) {
+        const float alpha = fast_exp2(m_run - m_tile);
+        l_run *= alpha;
+#pragma unroll
+        for (int i = 0; i < kDBlk; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+        m_run = m_tile;
       }
-    const float m_tile = fmaxf(mloc, shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, m_tile);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    float psum = 0.f;
+    }
+    const float nm = m_run == -INFINITY ? 0.f : -m_run;
     bf16x8 pb[4];
+    float l0 = 0.f, l1 = 0.f;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         bf16x8 v8;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = fast_exp2(sacc[blk][8 * j + e] - m_use);
-          psum += p;
-          v8[e] = (__bf16)p;
-        }
+        for (int e = 0; e < 8; ++e) v8[e] = (__bf16)fast_exp2(fmaf(sacc[blk][8 * j + e], c, nm));
         pb[blk * 2 + j] = v8;
+        // Row sums of the probabilities as rounded for the MFMA (bf16 pairs).
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+          l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[e], v8[e + 1]}, ones, l0, false);
+          l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[e + 2], v8[e + 3]}, ones, l1, false);
+        }
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < kDBlk; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+    l_run += l0 + l1;
 
-    // O^T += V^T P^T; the D/32 column blocks are independent chains, interleaved.
+    // O^T += V^T P^T; the D/32 column blocks are independent chains.
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int i = 0; i < kDBlk; ++i) {
         Pack8 va;
-        va.u = *reinterpret_cast<const uint4*>(&s_v[v_addr(i * 32 + col, ks * 16 + half * 8)]);
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const int row = 16 * ks + 8 * r + v_row_lane;
+          const int byte = G::offset(row, 4 * i + v_chunk_lane) + v_byte_lane;
+          va.h[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vt + byte));
+        }
         oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va.v, pb[ks], oacc[i], 0, 0, 0);
       }
     }
@@ -663,7 +685,15 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   for (int b = 0; b < batch; ++b)
     if (host_ctx_len[b] < 0 || host_n_nodes[b] < 0 || host_n_nodes[b] > n_max)
       return CURE_ERR_INVALID_ARG;
-  const bool mfma = use_mfma(dtype, d, flags);
+  // The MFMA kernel takes the row maximum on raw scores (valid for scale > 0)
+  // and addresses a sequence's K/V rows with 32-bit byte offsets.
+  bool mfma = use_mfma(dtype, d, flags) && scale > 0.f && std::isfinite(scale);
+  if (mfma) {
+    int64_t t_max = 0;
+    for (int b = 0; b < batch; ++b)
+      t_max = std::max<int64_t>(t_max, (int64_t)host_ctx_len[b] + host_n_nodes[b]);
+    if ((t_max + kTile) * hkv * d * 2 >= (int64_t(1) << 31)) mfma = false;
+  }
   const Plan p = make_plan(batch, hq, hkv, d, n_max, host_ctx_len, host_n_nodes, kv_split, mfma);
   if (p.max_splits == 0) return CURE_OK;    // no sequence has tree nodes
   const size_t need = plan_workspace(p, batch, hq, d, n_max);

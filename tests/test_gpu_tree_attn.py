@@ -13,7 +13,7 @@ import torch
 
 import paper_2608_00531_amd as pc
 from synth import preset, make_workload
-from parity_util import say, upload, gpu_attn, oracle_attn, check_attn, Timer
+from parity_util import say, upload, gpu_attn, oracle_attn, check_attn, Timer, LSE_TOL
 
 pytestmark = pytest.mark.gpu
 
@@ -53,10 +53,13 @@ def test_split_count_invariance(kv_split):
     ref_o, ref_l = oracle_attn(w)
     check_attn(w, o, lse, ref_o, ref_l)
     # Against the single-split result: splitting changes only where the bf16
-    # rounding of the probabilities happens, so the two agree to the bf16 bar.
+    # rounding of the probabilities (and of their row sums, which are taken on
+    # the rounded values the MFMA consumes) happens, so the two agree to the
+    # bf16 bars the oracle comparison uses.
     o1, l1, _ = gpu_attn(w, dev, out_dtype=torch.float32, kv_split=1)
     torch.cuda.synchronize()
-    assert float((o - o1).abs().max()) < 2e-3 and float((lse - l1).abs().max()) < 1e-4
+    assert float((o - o1).abs().max()) < 2e-3
+    assert float((lse - l1).abs().max()) < LSE_TOL["bf16"]
 
 
 @pytest.mark.parametrize("ctx", [0, 1, 63, 64, 65, 127, 128, 700])
@@ -161,3 +164,14 @@ def test_long_context_full_size_sampled():
     with Timer("oracle"):
         ref_o, ref_l = oracle_attn(w, sample=sample)
     check_attn(w, o, lse, ref_o, ref_l, sample=sample)
+
+
+def test_nonpositive_scale_takes_the_general_path():
+    say("attn negative scale")
+    w = make_workload("n", batch=2, hq=8, hkv=2, ctx_lens=[300, 71], chain_len=8, n_ufp=2,
+                      branch_depth=2, seed=44, scale=-0.05)
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle_attn(w)
+    check_attn(w, o, lse, ref_o, ref_l)
