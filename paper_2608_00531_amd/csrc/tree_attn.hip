@@ -281,6 +281,30 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// A buffer resource as four wave-uniform dwords (SGPRs).
+CURE_DEV i32x4 as_i32x4(__amdgpu_buffer_rsrc_t r) {
+  i32x4 v;
+  __builtin_memcpy(&v, &r, sizeof(v));
+  return i32x4{__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
+               __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w)};
+}
+
+CURE_DEV uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_void*)p);
+}
+
+// 64 lanes x 16 bytes from a buffer resource straight into LDS: lane i's bytes
+// land at lds_base + 16 * i (lds_base travels in M0). Out-of-range offsets
+// read as zero.
+CURE_DEV void dma16(uint32_t lds_base, uint32_t voff, i32x4 rsrc) {
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "{m0}"(lds_base)
+               : "memory");
+}
+
 union Pack8 {
   uint4 u;
   bf16x8 v;
@@ -296,12 +320,13 @@ struct TileGeo {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kTileBytes = kTile * kRowBytes;
   static constexpr int kBlocks = kTileBytes / 1024;  // 1 KB DMA blocks per tile
-  // Swizzle: the chunk index is XORed with a row-dependent value so that 16
-  // consecutive rows use 16 different chunk slots, and 4 consecutive rows
-  // (starting at a multiple of 4) keep their chunk pairs aligned.
+  // Swizzle: the chunk index is XORed with a row-dependent value so that any 8
+  // (head dim 64) or 16 (head dim 128) consecutive aligned rows read by the K
+  // operand land in distinct chunk slots, while the 4 aligned rows of one
+  // transposed V read keep bit 0 fixed and so occupy 4 distinct chunk pairs.
   static CURE_DEV int swz(int row) {
-    constexpr int h = kChunks / 2;
-    return ((row & (h - 1)) << 1) | ((row / h) & 1);
+    const int s = ((row & 3) << 1) | ((row >> 2) & 1);
+    return kChunks == 16 ? (s | (row & 8)) : s;
   }
   static CURE_DEV int offset(int row, int chunk) {   // byte offset inside a tile
     return row * kRowBytes + ((chunk ^ swz(row)) << 4);
@@ -332,10 +357,6 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   const int S = split_count(T, N, a.tps, a.max_splits);
   const int rows = N * a.group;
   if (s >= S || rb * a.rows_per_wg >= rows) return;
-  const bool reporter = s == 0 && hk == 0 && rb == 0;
-  const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
-  report_tree(a, b, ok, reporter);
-  if (!ok) return;
 
   const int begin = s * a.tps;
   const int end = (s == S - 1) ? T : begin + a.tps;
@@ -362,13 +383,19 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
     src_off[j] = (uint32_t)((row * a.hkv + hk) * G::kRowBytes + (lchunk << 4));
   }
   const uint32_t tok_bytes = (uint32_t)(a.hkv * G::kRowBytes);
+  // The DMA is issued from inline assembly on purpose: written through the
+  // compiler builtin, every later LDS read of the *current* tile gets a wait on
+  // the *next* tile's DMA (the compiler cannot tell the buffers apart), which
+  // serialises the pipeline. Ordering is explicit instead: each loop iteration
+  // starts with s_waitcnt + barrier before any LDS read of the tile it uses.
+  const i32x4 rk4 = as_i32x4(rk), rv4 = as_i32x4(rv);
   auto dma_tile = [&](int buf, int t0) {
 #pragma unroll
     for (int j = 0; j < kDmaPerWave; ++j) {
       const uint32_t voff = src_off[j] + (uint32_t)t0 * tok_bytes;
       const int blk = (wave * kDmaPerWave + j) * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(&s_k[buf][blk]), 16, (int)voff, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(&s_v[buf][blk]), 16, (int)voff, 0, 0, 0);
+      dma16(lds_addr(&s_k[buf][blk]), voff, rk4);
+      dma16(lds_addr(&s_v[buf][blk]), voff, rv4);
     }
   };
 
@@ -408,6 +435,17 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   const int v_chunk_lane = 2 * g16 + ((j16 & 3) >> 1);   // + 4*i
   const int v_byte_lane = (j16 & 1) * 8;
 
+  // The first tile's DMA and the query loads are in flight while the tree's
+  // ancestor masks are built.
+  dma_tile(0, begin);
+  const bool reporter = s == 0 && hk == 0 && rb == 0;
+  const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
+  report_tree(a, b, ok, reporter);
+  if (!ok) {
+    __builtin_amdgcn_s_waitcnt(0);        // no DMA may land after the workgroup ends
+    return;
+  }
+
   f32x16 oacc[kDBlk];
 #pragma unroll
   for (int i = 0; i < kDBlk; ++i)
@@ -417,7 +455,6 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   const float c = a.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  dma_tile(0, begin);
   int buf = 0;
   for (int t0 = begin; t0 < end; t0 += kTile, buf ^= 1) {
     __builtin_amdgcn_s_waitcnt(0);        // this wave's DMA into `buf` has landed
@@ -433,14 +470,22 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[blk][r] = 0.f;
+    // K operands are read one k-step ahead of the MFMAs that consume them.
+    Pack8 ka[2][2];
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+      ka[0][blk].u = *reinterpret_cast<const uint4*>(kt + k_row_base[blk] + (k_swz[blk] << 4));
 #pragma unroll
     for (int kk = 0; kk < kKSteps; ++kk) {
+      if (kk + 1 < kKSteps) {
 #pragma unroll
-      for (int blk = 0; blk < 2; ++blk) {
-        Pack8 ka;
-        ka.u = *reinterpret_cast<const uint4*>(kt + k_row_base[blk] + (((2 * kk) ^ k_swz[blk]) << 4));
-        sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka.v, qreg[kk], sacc[blk], 0, 0, 0);
+        for (int blk = 0; blk < 2; ++blk)
+          ka[(kk + 1) & 1][blk].u = *reinterpret_cast<const uint4*>(
+              kt + k_row_base[blk] + (((2 * (kk + 1)) ^ k_swz[blk]) << 4));
       }
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk)
+        sacc[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kk & 1][blk].v, qreg[kk], sacc[blk], 0, 0, 0);
     }
     // Mask the tail, then the tile's row maximum (raw units; the scale is > 0).
     if (t0 + kTile > L) {
