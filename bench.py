@@ -18,8 +18,12 @@ kernel, so host launch cost stays off the GPU timeline) to give the per-call
 durations used for the roofline.
 
 The printed JSON line's `value` is the step's algorithmic bytes over its time
-(GB/s). `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload on this host.
+(GB/s). `roofline` reports the longest call against the HBM peak; its
+`traffic` is the calibrated FETCH_SIZE + WRITE_SIZE bytes per call stored in
+profiles/traffic_<workload>.json, or null when that file is missing or the
+call's kernel sources have changed since the counters were taken.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload
+on this host.
 """
 
 import argparse
@@ -40,6 +44,11 @@ METRIC = "tree-verify step latency (µs) + KV GB/s vs HBM peak, Llama-3-8B attn 
 HBM_PEAK_GBS = 8000.0
 DEFAULT_WORKLOAD = "llama3_8b_ctx2k_b1"
 ROTATE_BYTES = 512 << 20
+CSRC = os.path.join(ROOT, "paper_2608_00531_amd", "csrc")
+# Kernel sources behind each call: a stored traffic figure is used only while
+# these files are unchanged since the counters were taken.
+CALL_SOURCES = {"margins": ["margins.hip", "common.hpp"], "attn": ["tree_attn.hip", "common.hpp"],
+                "accept": ["accept.hip", "common.hpp"]}
 
 
 def parse():
@@ -203,6 +212,25 @@ def per_call_times(torch, steps, k):
     return out
 
 
+def stored_traffic(call, workload):
+    """HBM bytes per call from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary
+    (calibrated against a plain copy), or None when there is none for this workload
+    or the call's kernel sources changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        entry = json.load(f).get("calls", {}).get(call)
+    if not entry:
+        return None
+    h = hashlib.sha256()
+    for name in CALL_SOURCES[call]:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return int(entry["bytes_per_call"]) if h.hexdigest() == entry["sources_sha256"] else None
+
+
 def cpu_baseline(w, algo_bytes, budget_s):
     import oracle
     try:
@@ -305,7 +333,8 @@ def main():
         "kernels": kernels,
         "roofline": {"bound": "hbm", "kernel": names[dom], "achieved": round(dom_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": stored_traffic(dom, w.name)},
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)
