@@ -47,26 +47,25 @@ CURE_DEV bool beats(float va, int ia, float vb, int ib) {
 
 CURE_DEV Top2 top2_empty() { return {-INFINITY, -INFINITY, INT32_MAX, INT32_MAX}; }
 
+// Both updates are written as value selects: a branchy form leads the
+// compiler to pick between the two records through a private-memory copy.
 CURE_DEV void top2_push(Top2& t, float x, int i) {
-  if (beats(x, i, t.v1, t.i1)) {
-    t.v2 = t.v1; t.i2 = t.i1; t.v1 = x; t.i1 = i;
-  } else if (beats(x, i, t.v2, t.i2)) {
-    t.v2 = x; t.i2 = i;
-  }
+  const bool c1 = beats(x, i, t.v1, t.i1);
+  const bool c2 = !c1 && beats(x, i, t.v2, t.i2);
+  t.v2 = c1 ? t.v1 : (c2 ? x : t.v2);
+  t.i2 = c1 ? t.i1 : (c2 ? i : t.i2);
+  t.v1 = c1 ? x : t.v1;
+  t.i1 = c1 ? i : t.i1;
 }
 
+// The winner's first entry, then the better of the loser's first entry and
+// the winner's second.
 CURE_DEV Top2 top2_merge(const Top2& a, const Top2& b) {
-  Top2 r;
-  if (beats(b.v1, b.i1, a.v1, a.i1)) {
-    r.v1 = b.v1; r.i1 = b.i1;
-    if (beats(a.v1, a.i1, b.v2, b.i2)) { r.v2 = a.v1; r.i2 = a.i1; }
-    else { r.v2 = b.v2; r.i2 = b.i2; }
-  } else {
-    r.v1 = a.v1; r.i1 = a.i1;
-    if (beats(b.v1, b.i1, a.v2, a.i2)) { r.v2 = b.v1; r.i2 = b.i1; }
-    else { r.v2 = a.v2; r.i2 = a.i2; }
-  }
-  return r;
+  const bool bw = beats(b.v1, b.i1, a.v1, a.i1);
+  const float w1 = bw ? b.v1 : a.v1, w2 = bw ? b.v2 : a.v2, l1 = bw ? a.v1 : b.v1;
+  const int wi1 = bw ? b.i1 : a.i1, wi2 = bw ? b.i2 : a.i2, li1 = bw ? a.i1 : b.i1;
+  const bool lw = beats(l1, li1, w2, wi2);
+  return {w1, lw ? l1 : w2, wi1, lw ? li1 : wi2};
 }
 
 CURE_DEV Top2 top2_wave_reduce(Top2 t) {

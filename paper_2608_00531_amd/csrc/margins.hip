@@ -32,7 +32,7 @@ constexpr int kThreads = 256;
 constexpr int kVec = 8;            // entries per lane per vector step
 constexpr int kUnroll = 2;         // vector steps per lane per loop step
 constexpr int kMaxSplits = 32;
-constexpr int kMinChunk = 8192;    // entries per workgroup, at least
+constexpr int kMinChunk = 8192;    // entries per workgroup, about
 constexpr int kTargetWgsPerCu = 2;
 constexpr int kMaxGateChain = 1024;
 constexpr float kRescaleAt = 16.f; // re-reference the exp sum when a value exceeds ref + 16
@@ -135,10 +135,9 @@ CURE_DEV void write_row(const Args& a, int row, const Top2& t, float lse) {
 }
 
 // UFP selection for sequence b: candidates m < tau, ranked by (m, position).
-CURE_DEV void select_ufp(const Args& a, int b, float* sm) {
+// sm holds the sequence's first chain_len margins (LDS, filled by the caller).
+CURE_DEV void select_ufp(const Args& a, int b, const float* sm) {
   const int K = a.chain_len;
-  for (int i = threadIdx.x; i < K; i += kThreads) sm[i] = a.margin[(int64_t)b * a.rows + i];
-  __syncthreads();
   int local = 0;
   for (int i = threadIdx.x; i < K; i += kThreads) {
     const float mi = sm[i];
@@ -301,62 +300,43 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
 // Per sequence: merge each row's chunk results (when rows were split), then
 // select the sequence's UFPs from its chain rows' margins.
 //
-// Lanes are grouped G = splits rounded up to a power of two: each group holds
-// one row's chunk results, one per lane, and reduces them with xor shuffles
-// inside the group. kFinishUnroll passes of rows are loaded before any is
-// reduced, so a sequence costs one memory round trip per 4 * kFinishUnroll *
-// (64 / G) rows.
-constexpr int kFinishUnroll = 4;
-
-CURE_DEV Top2 top2_group_reduce(Top2 t, int group) {
-  for (int m = group >> 1; m >= 1; m >>= 1) {
-    Top2 o;
-    o.v1 = shfl_xor(t.v1, m); o.i1 = shfl_xor(t.i1, m);
-    o.v2 = shfl_xor(t.v2, m); o.i2 = shfl_xor(t.i2, m);
-    t = top2_merge(t, o);
-  }
-  return t;
-}
-
-CURE_DEV Lse lse_group_reduce(Lse s, int group) {
-  for (int m = group >> 1; m >= 1; m >>= 1) s = lse_merge(s, Lse{shfl_xor(s.ref, m), shfl_xor(s.sum, m)});
-  return s;
-}
+// One thread per row. A row's chunk results are contiguous; a thread issues
+// the loads of kFinishBatch of them before merging any, so a row with up to
+// kFinishBatch chunks costs one memory round trip. The chain rows' margins go
+// to LDS as they are produced, so the gate needs no second trip to memory.
+constexpr int kFinishBatch = 16;
 
 __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
   __shared__ float s_margin[kMaxGateChain];
   const int b = blockIdx.x;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   if (a.splits > 1) {
-    int group = 1;
-    while (group < a.splits) group <<= 1;               // splits <= kMaxSplits <= 64
-    const int per_wave = kWave / group;
-    const int per_pass = per_wave * (kThreads / kWave);
-    const int sp = lane & (group - 1);
-    const int r_in_pass = wave * per_wave + lane / group;
-    for (int r0 = 0; r0 < a.rows; r0 += per_pass * kFinishUnroll) {
-      Partial q[kFinishUnroll];
+    for (int r = threadIdx.x; r < a.rows; r += kThreads) {
+      const Partial* p = a.partials + ((int64_t)b * a.rows + r) * a.splits;
+      Top2 t = top2_empty();
+      Lse ls{kLseEmptyRef, 0.f};
+      for (int s0 = 0; s0 < a.splits; s0 += kFinishBatch) {
+        Partial q[kFinishBatch];
 #pragma unroll
-      for (int u = 0; u < kFinishUnroll; ++u) {
-        const int r = r0 + u * per_pass + r_in_pass;
-        q[u] = Partial{kLseEmptyRef, 0.f, -INFINITY, -INFINITY, INT32_MAX, INT32_MAX, 0, 0};
-        if (r < a.rows && sp < a.splits)
-          q[u] = a.partials[((int64_t)b * a.rows + r) * a.splits + sp];
-      }
+        for (int u = 0; u < kFinishBatch; ++u)
+          if (s0 + u < a.splits) q[u] = p[s0 + u];
 #pragma unroll
-      for (int u = 0; u < kFinishUnroll; ++u) {
-        const int r = r0 + u * per_pass + r_in_pass;
-        const Top2 t = top2_group_reduce(Top2{q[u].v1, q[u].v2, q[u].i1, q[u].i2}, group);
-        const Lse ls = lse_group_reduce(Lse{q[u].ref, q[u].sum}, group);
-        if (sp == 0 && r < a.rows) write_row(a, b * a.rows + r, t, lse_value(ls));
+        for (int u = 0; u < kFinishBatch; ++u)
+          if (s0 + u < a.splits) {
+            t = top2_merge(t, Top2{q[u].v1, q[u].v2, q[u].i1, q[u].i2});
+            ls = lse_merge(ls, Lse{q[u].ref, q[u].sum});
+          }
       }
+      write_row(a, b * a.rows + r, t, lse_value(ls));
+      if (r < a.chain_len) s_margin[r] = t.v1 - t.v2;
     }
-    if (a.ufp_pos) {
-      __threadfence_block();
-      __syncthreads();
-    }
+  } else if (a.ufp_pos) {
+    for (int i = threadIdx.x; i < a.chain_len; i += kThreads)
+      s_margin[i] = a.margin[(int64_t)b * a.rows + i];
   }
-  if (a.ufp_pos) select_ufp(a, b, s_margin);
+  if (a.ufp_pos) {
+    __syncthreads();
+    select_ufp(a, b, s_margin);
+  }
 }
 
 }  // namespace
@@ -393,10 +373,12 @@ extern "C" cure_status cure_margins(const void* logits, int32_t dtype, int32_t b
   const int64_t nrow = (int64_t)batch * rows;
   if (nrow > INT32_MAX / kMaxSplits) return CURE_ERR_UNSUPPORTED;
 
-  // Enough workgroups to cover the GPU several times over, each chunk at
-  // least kMinChunk entries.
+  // Enough workgroups to cover the GPU kTargetWgsPerCu times over, with chunks
+  // of about kMinChunk entries or more: at most ceil(vocab / kMinChunk) splits,
+  // so a small batch's chunk fits one loop step of each register set (all its
+  // loads in flight at once).
   int splits = (int)((kTargetWgsPerCu * (int64_t)device_cu_count() + nrow - 1) / nrow);
-  splits = std::max(1, std::min(splits, std::min(kMaxSplits, vocab / kMinChunk)));
+  splits = std::max(1, std::min(splits, std::min(kMaxSplits, (vocab + kMinChunk - 1) / kMinChunk)));
   int chunk = (vocab + splits - 1) / splits;
   chunk = (chunk + kVec - 1) / kVec * kVec;
   splits = (vocab + chunk - 1) / chunk;

@@ -594,8 +594,20 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
 
 // ---------------------------------------------------------------------------
 // LSE merge: one wave per output row (b, n, head).
+//
+// A split's partial row is D floats = D/4 lanes of float4, so one load
+// instruction covers 64/(D/4) splits (2 at D=128, 4 at D=64). A batch of
+// kMergeBatch such loads, with each split's LSE alongside, is issued before
+// anything is reduced: for up to 16 (D=128) or 32 (D=64) splits the whole
+// merge is a single memory round trip. The lane groups holding different
+// splits are combined with xor shuffles at the end.
+constexpr int kMergeBatch = 8;
+
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
+  constexpr int kLanesPerSplit = D / 4;
+  constexpr int kSplitsPerLoad = kWave / kLanesPerSplit;
+  constexpr int kSplitsPerBatch = kSplitsPerLoad * kMergeBatch;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
   const int64_t nrows = (int64_t)batch * a.n_max * a.hq;
@@ -608,24 +620,59 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   const int S = split_count(a.ctx_len[b] + N, N, a.tps, a.max_splits);
   if (S <= 1) return;
   const int64_t p0 = part_index(a, b, head, n, 0);
+  const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
+  const int col = (lane % kLanesPerSplit) * 4;      // its four output columns
+
+  float4 v[kMergeBatch];
+  float l[kMergeBatch];
+  auto load_batch = [&](int s0) {
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const int sp = s0 + u * kSplitsPerLoad + sub;
+      const bool ok = sp < S;
+      v[u] = ok ? *reinterpret_cast<const float4*>(a.part_o + (p0 + sp) * D + col)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+      l[u] = ok ? a.part_lse[p0 + sp] : -INFINITY;
+    }
+  };
+  load_batch(0);
   float m = -INFINITY;
-  for (int s = lane; s < S; s += 64) m = fmaxf(m, a.part_lse[p0 + s]);
+  for (int sp = lane; sp < S; sp += kWave) m = fmaxf(m, a.part_lse[p0 + sp]);
 #pragma unroll
   for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor(m, k));
-  float acc[D / 64] = {};
+  const float ms = m == -INFINITY ? 0.f : m;     // empty splits (lse = -inf) weigh 0
+
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float wsum = 0.f;
-  if (m != -INFINITY) {
-    for (int s = 0; s < S; ++s) {
-      const float w = __expf(a.part_lse[p0 + s] - m);
+  for (int s0 = 0;;) {
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const float w = fast_exp2((l[u] - ms) * kLog2e);
       wsum += w;
-#pragma unroll
-      for (int c = 0; c < D / 64; ++c) acc[c] = fmaf(w, a.part_o[(p0 + s) * D + lane + 64 * c], acc[c]);
+      acc.x = fmaf(w, v[u].x, acc.x);
+      acc.y = fmaf(w, v[u].y, acc.y);
+      acc.z = fmaf(w, v[u].z, acc.z);
+      acc.w = fmaf(w, v[u].w, acc.w);
     }
+    s0 += kSplitsPerBatch;
+    if (s0 >= S) break;
+    load_batch(s0);
   }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
 #pragma unroll
-  for (int c = 0; c < D / 64; ++c) store_out(a, obase + lane + 64 * c, acc[c] * inv);
+  for (int k = kLanesPerSplit; k < kWave; k <<= 1) {
+    acc.x += shfl_xor(acc.x, k);
+    acc.y += shfl_xor(acc.y, k);
+    acc.z += shfl_xor(acc.z, k);
+    acc.w += shfl_xor(acc.w, k);
+    wsum += shfl_xor(wsum, k);
+  }
+  if (sub != 0) return;
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D + col;
+  store_out(a, obase, acc.x * inv);
+  store_out(a, obase + 1, acc.y * inv);
+  store_out(a, obase + 2, acc.z * inv);
+  store_out(a, obase + 3, acc.w * inv);
   if (lane == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] =
       wsum > 0.f ? m + logf(wsum) : -INFINITY;
 }

@@ -73,7 +73,7 @@ def test_edge_rows(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("vocab", [3, 7, 8, 9, 255, 2049, 8193, 40001, 128256])
+@pytest.mark.parametrize("vocab", [3, 7, 8, 9, 255, 2049, 8193, 40001, 128256, 262147])
 def test_random_rows_many_vocab_sizes(dtype, vocab):
     say("margins random rows vocab", vocab, dtype)
     rng = np.random.default_rng(vocab)

@@ -109,15 +109,18 @@ def test_row_blocking_and_wide_trees(hq, hkv, n_ufp, depth):
         check_attn(w, o, lse, ref_o, ref_l)
 
 
-def test_head_dim_64_bf16():
-    say("attn d64")
-    w = make_workload("d", batch=2, hq=16, hkv=4, d=64, ctx_lens=[400, 1300], chain_len=12,
+@pytest.mark.parametrize("kv_split", [0, 3, 60])
+def test_head_dim_64_bf16(kv_split):
+    # 60 requested splits give 42 (64-token splits) on the long sequence: more
+    # than one batch of merge loads at D = 64.
+    say("attn d64 kv_split", kv_split)
+    w = make_workload("d", batch=2, hq=16, hkv=4, d=64, ctx_lens=[400, 2600], chain_len=12,
                       n_ufp=3, branch_depth=2, seed=99)
     dev = upload(w)
+    ref_o, ref_l = oracle_attn(w)
     for flags in (0, pc.CURE_ATTN_FORCE_VALU):
-        o, lse, st = gpu_attn(w, dev, flags=flags)
+        o, lse, st = gpu_attn(w, dev, flags=flags, kv_split=kv_split)
         torch.cuda.synchronize()
-        ref_o, ref_l = oracle_attn(w)
         check_attn(w, o, lse, ref_o, ref_l)
 
 
