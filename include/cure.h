@@ -124,9 +124,9 @@ cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch, int32
  *   host_ctx_len/host_n_nodes: host copies of ctx_len/n_nodes, used only to
  *           plan the split of each context across workgroups.
  * Rows n >= n_nodes[b] of o and lse are not written.
- * tree_status [batch] int32 (may be NULL): CURE_OK, or CURE_ERR_BAD_TREE when
- * sequence b's parent array is malformed (that sequence's o/lse are then
- * unspecified).
+ * tree_status [batch] int32 (may be NULL): CURE_OK (also for a sequence with
+ * no nodes), or CURE_ERR_BAD_TREE when sequence b's parent array is malformed
+ * (that sequence's o/lse are then unspecified).
  * Supports d in {64, 128}, hq % hkv == 0, 0 <= n_nodes[b] <= min(n_max, 256)
  * (a sequence with no nodes is skipped).
  * kv_split: 0 = automatic, else the number of context splits per sequence.

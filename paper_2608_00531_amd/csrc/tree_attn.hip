@@ -36,6 +36,7 @@ namespace cure {
 namespace {
 
 constexpr int kTile = 64;            // tokens per K/V tile
+constexpr int kStages = 2;           // K/V tile buffers in the MFMA kernel's LDS ring
 constexpr int kMinTps = 256;         // tokens per split, at least
 constexpr int kAncWords = CURE_MAX_TREE_NODES / 64;
 
@@ -142,6 +143,10 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
   const int T = L + N;
   const int S = split_count(T, N, a.tps, a.max_splits);
   const int rows = N * a.group;
+  if (S == 0) {                         // no nodes: nothing to compute; the empty tree is valid
+    report_tree(a, b, true, s == 0 && hk == 0 && rb == 0);
+    return;
+  }
   if (s >= S || rb * kValuRows >= rows) return;
   const bool reporter = s == 0 && hk == 0 && rb == 0;
   const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
@@ -268,12 +273,16 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
 //   online softmax in the log2 domain, rescaling O only when a row's maximum
 //   rises by more than 2^8 (values then stay below 2^8, safe in bf16 and fp32)
 //   O^T += V^T P^T (D/32 column blocks x 4 k-steps)
-// K and V tiles move HBM -> LDS by DMA (buffer loads that write LDS directly),
-// double-buffered so the next tile streams in while this one is computed. The
-// per-sequence buffer resource bounds every read: rows past the sequence end
-// read as zeros. LDS rows are 16-byte-chunk XOR-swizzled so that both the K
-// reads (one row per lane) and the transposed V reads (4 rows x 16 columns per
-// 16 lanes, ds_read_b64_tr_b16) spread over the banks.
+// K and V tiles move HBM -> LDS by DMA (buffer loads that write LDS directly)
+// through a ring of NBUF tile buffers: while one tile is computed, the next
+// NBUF - 1 stream in. Two buffers at head dim 128 leave room for two
+// workgroups (eight waves) per CU; a deeper ring trades those waves for more
+// bytes in flight, and measured slower. The per-sequence buffer resource
+// bounds every read: rows past the sequence end read as zeros, and ring
+// slots past the split's end are filled by reads at an offset past the
+// resource, which touch no memory. LDS rows are 16-byte-chunk XOR-swizzled so
+// that both the K reads (one row per lane) and the transposed V reads (4 rows
+// x 16 columns per 16 lanes, ds_read_b64_tr_b16) spread over the banks.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -333,34 +342,53 @@ struct TileGeo {
   }
 };
 
-template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
+// s_waitcnt immediate: at most `vm` vector-memory operations outstanding, no
+// wait on export, all LDS/scalar-memory operations complete (gfx9 encoding:
+// vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14, expcnt in 6:4).
+constexpr int waitcnt_vm(int vm) { return (vm & 15) | ((vm >> 4) << 14) | (7 << 4); }
+constexpr uint32_t kOobOffset = 0x80000000u;   // past any sequence's buffer resource
+
+template <int D, int NW, int NBUF>
+__global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args a) {
   using G = TileGeo<D>;
   constexpr int kKSteps = D / 16;                  // MFMA k-steps for Q K^T
   constexpr int kDBlk = D / 32;                    // 32-column blocks of O^T
   constexpr int kDmaPerWave = G::kBlocks / NW;     // DMA blocks per wave per tensor
+  // Each loop iteration waits until its tile has landed while the NBUF - 2
+  // tiles issued after it may still be in flight (2 instructions per block).
+  constexpr int kVmWait = waitcnt_vm((NBUF - 2) * 2 * kDmaPerWave);
+  static_assert((NBUF - 2) * 2 * kDmaPerWave < 64, "vmcnt holds 6 bits");
   static_assert(G::kBlocks % NW == 0, "tile must split evenly across waves");
 
   __shared__ int s_parent[CURE_MAX_TREE_NODES];
   __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
   __shared__ int s_bad;
-  __shared__ __attribute__((aligned(1024))) unsigned char s_k[2][G::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char s_v[2][G::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_k[NBUF][G::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_v[NBUF][G::kTileBytes];
 
   const int b = blockIdx.z;
   const int hk = blockIdx.y % a.hkv;
   const int rb = blockIdx.y / a.hkv;
   const int s = blockIdx.x;
-  const int N = min(a.n_nodes[b], a.n_max);
+  // The sequence's sizes and cache offset are independent loads: one round
+  // trip. The empty asm keeps the compiler from sinking the offset's load
+  // below the early exits (a second round trip).
+  const int n_raw = a.n_nodes[b];
   const int L = a.ctx_len[b];
+  const int64_t off = a.kv_off[b];
+  asm volatile("" : : "s"(n_raw), "s"(L), "s"(off));
+  const int N = min(n_raw, a.n_max);
   const int T = L + N;
   const int S = split_count(T, N, a.tps, a.max_splits);
   const int rows = N * a.group;
+  if (S == 0) {                         // no nodes: nothing to compute; the empty tree is valid
+    report_tree(a, b, true, s == 0 && hk == 0 && rb == 0);
+    return;
+  }
   if (s >= S || rb * a.rows_per_wg >= rows) return;
 
   const int begin = s * a.tps;
   const int end = (s == S - 1) ? T : begin + a.tps;
-  const int64_t off = a.kv_off[b];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
 
@@ -388,16 +416,23 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   // the *next* tile's DMA (the compiler cannot tell the buffers apart), which
   // serialises the pipeline. Ordering is explicit instead: each loop iteration
   // starts with s_waitcnt + barrier before any LDS read of the tile it uses.
+  // A tile at or past the split's end is still issued (at an out-of-range
+  // offset) so that every iteration has the same number of DMAs in flight.
   const i32x4 rk4 = as_i32x4(rk), rv4 = as_i32x4(rv);
   auto dma_tile = [&](int buf, int t0) {
+    const bool live = t0 < end;
 #pragma unroll
     for (int j = 0; j < kDmaPerWave; ++j) {
-      const uint32_t voff = src_off[j] + (uint32_t)t0 * tok_bytes;
+      const uint32_t voff = live ? src_off[j] + (uint32_t)t0 * tok_bytes : kOobOffset;
       const int blk = (wave * kDmaPerWave + j) * 1024;
       dma16(lds_addr(&s_k[buf][blk]), voff, rk4);
       dma16(lds_addr(&s_v[buf][blk]), voff, rv4);
     }
   };
+
+  // The first tiles' DMA goes out before anything else this workgroup loads.
+#pragma unroll
+  for (int i = 0; i < NBUF - 1; ++i) dma_tile(i, begin + i * kTile);
 
   // This lane's query row.
   const int R = rb * a.rows_per_wg + wave * 32 + col;
@@ -435,15 +470,17 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   const int v_chunk_lane = 2 * g16 + ((j16 & 3) >> 1);   // + 4*i
   const int v_byte_lane = (j16 & 1) * 8;
 
-  // The first tile's DMA and the query loads are in flight while the tree's
-  // ancestor masks are built.
-  dma_tile(0, begin);
-  const bool reporter = s == 0 && hk == 0 && rb == 0;
-  const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
-  report_tree(a, b, ok, reporter);
-  if (!ok) {
-    __builtin_amdgcn_s_waitcnt(0);        // no DMA may land after the workgroup ends
-    return;
+  // Only a split that reaches the tree's own rows needs the ancestor masks
+  // (built while the first tile and the queries are in flight). The last
+  // split always does, and it reports the tree's status. With a malformed
+  // tree the other splits still run; the sequence's output is unspecified.
+  if (end > L) {
+    const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
+    report_tree(a, b, ok, s == S - 1 && hk == 0 && rb == 0);
+    if (!ok) {
+      __builtin_amdgcn_s_waitcnt(0);      // no DMA may land after the workgroup ends
+      return;
+    }
   }
 
   f32x16 oacc[kDBlk];
@@ -455,11 +492,13 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
   const float c = a.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  int buf = 0;
-  for (int t0 = begin; t0 < end; t0 += kTile, buf ^= 1) {
-    __builtin_amdgcn_s_waitcnt(0);        // this wave's DMA into `buf` has landed
-    __syncthreads();                      // everyone's has; `buf ^ 1` is free again
-    if (t0 + kTile < end) dma_tile(buf ^ 1, t0 + kTile);
+  // Queries and the first tiles have landed. (This also tells the compiler
+  // that no load it issued is pending, so it adds no waits inside the loop.)
+  __builtin_amdgcn_s_waitcnt(0);
+  for (int t0 = begin, buf = 0; t0 < end; t0 += kTile, buf = buf + 1 == NBUF ? 0 : buf + 1) {
+    __builtin_amdgcn_s_waitcnt(kVmWait);  // this wave's DMA into `buf` has landed
+    __syncthreads();                      // everyone's has; the previous buffer is free
+    dma_tile(buf == 0 ? NBUF - 1 : buf - 1, t0 + (NBUF - 1) * kTile);
     if (!wave_active) continue;
     const unsigned char* kt = s_k[buf];
     const unsigned char* vt = s_v[buf];
@@ -553,6 +592,7 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
     }
   }
 
+  __builtin_amdgcn_s_waitcnt(0);          // the ring's trailing DMAs land before exit
   if (!row_ok) return;
   const float l_tot = l_run + shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -596,18 +636,17 @@ __global__ __launch_bounds__(64 * NW, 2) void tree_attn_mfma(Args a) {
 // LSE merge: one wave per output row (b, n, head).
 //
 // A split's partial row is D floats = D/4 lanes of float4, so one load
-// instruction covers 64/(D/4) splits (2 at D=128, 4 at D=64). A batch of
-// kMergeBatch such loads, with each split's LSE alongside, is issued before
-// anything is reduced: for up to 16 (D=128) or 32 (D=64) splits the whole
-// merge is a single memory round trip. The lane groups holding different
-// splits are combined with xor shuffles at the end.
-constexpr int kMergeBatch = 8;
-
-template <int D>
+// instruction covers 64/(D/4) splits (2 at D=128, 4 at D=64). A batch of NB
+// such loads, with each split's LSE alongside, is issued before anything is
+// reduced, and NB is the smallest of 2, 4, 8 that covers the launch's largest
+// split count when it can: the whole merge is then one memory round trip,
+// with no more registers held than that needs. The lane groups holding
+// different splits are combined with xor shuffles at the end.
+template <int D, int NB>
 __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   constexpr int kLanesPerSplit = D / 4;
   constexpr int kSplitsPerLoad = kWave / kLanesPerSplit;
-  constexpr int kSplitsPerBatch = kSplitsPerLoad * kMergeBatch;
+  constexpr int kSplitsPerBatch = kSplitsPerLoad * NB;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
   const int64_t nrows = (int64_t)batch * a.n_max * a.hq;
@@ -615,19 +654,21 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   const int head = (int)(rowid % a.hq);
   const int n = (int)((rowid / a.hq) % a.n_max);
   const int b = (int)(rowid / ((int64_t)a.hq * a.n_max));
-  const int N = min(a.n_nodes[b], a.n_max);
+  const int n_raw = a.n_nodes[b];
+  const int L = a.ctx_len[b];
+  const int N = min(n_raw, a.n_max);
   if (n >= N) return;
-  const int S = split_count(a.ctx_len[b] + N, N, a.tps, a.max_splits);
+  const int S = split_count(L + N, N, a.tps, a.max_splits);
   if (S <= 1) return;
   const int64_t p0 = part_index(a, b, head, n, 0);
   const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
   const int col = (lane % kLanesPerSplit) * 4;      // its four output columns
 
-  float4 v[kMergeBatch];
-  float l[kMergeBatch];
+  float4 v[NB];
+  float l[NB];
   auto load_batch = [&](int s0) {
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) {
+    for (int u = 0; u < NB; ++u) {
       const int sp = s0 + u * kSplitsPerLoad + sub;
       const bool ok = sp < S;
       v[u] = ok ? *reinterpret_cast<const float4*>(a.part_o + (p0 + sp) * D + col)
@@ -646,7 +687,7 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   float wsum = 0.f;
   for (int s0 = 0;;) {
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) {
+    for (int u = 0; u < NB; ++u) {
       const float w = fast_exp2((l[u] - ms) * kLog2e);
       wsum += w;
       acc.x = fmaf(w, v[u].x, acc.x);
@@ -688,6 +729,18 @@ struct Plan {
   int max_splits;
 };
 
+// MFMA workgroups one CU holds at once: bounded by LDS (the K/V ring plus the
+// tree masks) and by registers (about 220 VGPRs per lane at head dim 128, so
+// two waves per SIMD; about 120 at head dim 64, four waves per SIMD).
+int mfma_wgs_per_cu(int d, int nw) {
+  constexpr int kLdsPerCu = 160 * 1024;
+  const int lds = 2 * kStages * kTile * d * 2 +
+                  CURE_MAX_TREE_NODES * (4 + kAncWords * 8) + 64;
+  const int by_lds = kLdsPerCu / lds;
+  const int by_regs = (d == 128 ? 8 : 16) / nw;
+  return std::max(1, std::min(by_lds, by_regs));
+}
+
 Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
                const int32_t* host_ctx_len, const int32_t* host_n_nodes, int32_t kv_split,
                bool mfma) {
@@ -711,15 +764,42 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
     t_max = std::max(t_max, T);
     t_sum += T;
   }
+  const auto round_tile = [](int64_t t) {
+    return std::max<int64_t>(kTile, (t + kTile - 1) / kTile * kTile);
+  };
+  // Workgroups of one launch: splits of every sequence x kv-heads x row blocks.
+  const auto workgroups = [&](int64_t tps) {
+    int64_t c = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int N = std::min(host_n_nodes[b], n_max);
+      if (N > 0) c += ((int64_t)host_ctx_len[b] + N + tps - 1) / tps;
+    }
+    return c * hkv * p.row_blocks;
+  };
   int64_t tps;
   if (kv_split > 0) {
-    tps = (t_max + kv_split - 1) / kv_split;
+    tps = round_tile((t_max + kv_split - 1) / kv_split);
   } else {
-    const int64_t target = 2LL * device_cu_count();
-    const int64_t work = t_sum * hkv * p.row_blocks;
-    tps = std::max<int64_t>(kMinTps, (work + target - 1) / std::max<int64_t>(1, target));
+    // The shortest split (at least kMinTps tokens) whose workgroups are all
+    // resident at once, so no workgroup waits for a second round. A batch with
+    // more sequence x head pairs than that gets a single split per sequence.
+    const int64_t slots = (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw) : 2) * device_cu_count();
+    const int64_t hi = round_tile(t_max);
+    int64_t lo = round_tile(std::max<int64_t>(
+        kMinTps, (t_sum * hkv * p.row_blocks + slots - 1) / std::max<int64_t>(1, slots)));
+    if (lo >= hi || workgroups(hi) > slots) {
+      tps = hi;
+    } else {
+      // workgroups() falls as tps grows: bisect over multiples of the tile.
+      int64_t a = lo / kTile, z = hi / kTile;       // workgroups(z * kTile) <= slots
+      while (a < z) {
+        const int64_t m = (a + z) / 2;
+        if (workgroups(m * kTile) <= slots) z = m;
+        else a = m + 1;
+      }
+      tps = z * kTile;
+    }
   }
-  tps = std::max<int64_t>(kTile, (tps + kTile - 1) / kTile * kTile);
   p.tps = (int)std::min<int64_t>(tps, INT32_MAX / 2);
   p.max_splits = t_max > 0 ? (int)((t_max + p.tps - 1) / p.tps) : 0;
   return p;
@@ -831,11 +911,11 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   const dim3 grid(p.max_splits, hkv * p.row_blocks, batch);
   if (mfma) {
     if (d == 128) {
-      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<128, 4>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((tree_attn_mfma<128, 8>), grid, dim3(512), 0, st, a);
+      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<128, 4, kStages>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_mfma<128, 8, kStages>), grid, dim3(512), 0, st, a);
     } else {
-      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<64, 4>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((tree_attn_mfma<64, 8>), grid, dim3(512), 0, st, a);
+      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<64, 4, kStages>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_mfma<64, 8, kStages>), grid, dim3(512), 0, st, a);
     }
   } else {
     if (dtype == CURE_BF16) {
@@ -850,8 +930,17 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   if (p.max_splits > 1) {
     const int64_t nrows = (int64_t)batch * n_max * hq;
     const dim3 mgrid((unsigned)((nrows + 3) / 4));
-    if (d == 128) hipLaunchKernelGGL((attn_merge<128>), mgrid, dim3(256), 0, st, a, batch);
-    else hipLaunchKernelGGL((attn_merge<64>), mgrid, dim3(256), 0, st, a, batch);
+    const int per_load = 256 / d;                       // splits per merge load
+    const int nb = p.max_splits <= 2 * per_load ? 2 : p.max_splits <= 4 * per_load ? 4 : 8;
+    if (d == 128) {
+      if (nb == 2) hipLaunchKernelGGL((attn_merge<128, 2>), mgrid, dim3(256), 0, st, a, batch);
+      else if (nb == 4) hipLaunchKernelGGL((attn_merge<128, 4>), mgrid, dim3(256), 0, st, a, batch);
+      else hipLaunchKernelGGL((attn_merge<128, 8>), mgrid, dim3(256), 0, st, a, batch);
+    } else {
+      if (nb == 2) hipLaunchKernelGGL((attn_merge<64, 2>), mgrid, dim3(256), 0, st, a, batch);
+      else if (nb == 4) hipLaunchKernelGGL((attn_merge<64, 4>), mgrid, dim3(256), 0, st, a, batch);
+      else hipLaunchKernelGGL((attn_merge<64, 8>), mgrid, dim3(256), 0, st, a, batch);
+    }
   }
   return launch_status();
 }

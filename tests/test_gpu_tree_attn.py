@@ -77,9 +77,9 @@ def test_context_lengths_around_tiles(ctx):
 
 def test_ragged_nodes_and_contexts():
     say("attn ragged")
-    w = make_workload("r", batch=5, ctx_lens=[300, 0, 1500, 64, 999], chain_len=16, n_ufp=4,
-                      branch_depth=4, seed=81)
-    w.n_nodes[:] = [32, 1, 20, 32, 17]               # prefixes of each tree are trees too
+    w = make_workload("r", batch=6, ctx_lens=[300, 0, 1500, 64, 999, 50], chain_len=16,
+                      n_ufp=4, branch_depth=4, seed=81)
+    w.n_nodes[:] = [32, 1, 20, 32, 17, 0]            # prefixes of each tree are trees too
     # Rebuild the cache layout for the shorter trees (rows past n_nodes are dropped).
     rows = w.ctx_len + w.n_nodes
     off = np.concatenate([[0], np.cumsum(rows)[:-1]]).astype(np.int64)
@@ -90,6 +90,7 @@ def test_ragged_nodes_and_contexts():
     for flags in (0, pc.CURE_ATTN_FORCE_VALU):
         o, lse, st = gpu_attn(w, dev, flags=flags)
         torch.cuda.synchronize()
+        assert st.tolist() == [pc.CURE_OK] * w.batch     # an empty tree is a valid tree
         ref_o, ref_l = oracle_attn(w)
         check_attn(w, o, lse, ref_o, ref_l)
 
