@@ -93,6 +93,29 @@ CURE_DEV bool build_tree(const Args& a, int b, int N, int* s_parent,
   return true;
 }
 
+// As build_tree, for a workgroup of at least N threads where thread n has
+// already loaded parent[n] (the load is issued early, off the critical path).
+CURE_DEV bool build_tree_loaded(int N, int my_parent, int* s_parent,
+                                unsigned long long (*s_anc)[kAncWords], int* s_bad) {
+  const int n = threadIdx.x;
+  if (n == 0) *s_bad = 0;
+  __syncthreads();
+  if (n < N) {
+    s_parent[n] = my_parent;
+    if (my_parent < -1 || my_parent >= n) *s_bad = 1;
+  }
+  __syncthreads();
+  if (*s_bad) return false;
+  if (n < N) {
+    unsigned long long w[kAncWords] = {};
+    for (int j = n; j >= 0; j = s_parent[j]) w[j >> 6] |= 1ull << (j & 63);
+#pragma unroll
+    for (int i = 0; i < kAncWords; ++i) s_anc[n][i] = w[i];
+  }
+  __syncthreads();
+  return true;
+}
+
 CURE_DEV void report_tree(const Args& a, int b, bool ok, bool reporter) {
   if (reporter && threadIdx.x == 0 && a.tree_status) a.tree_status[b] = ok ? CURE_OK : CURE_ERR_BAD_TREE;
 }
@@ -370,6 +393,31 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
   const int hk = blockIdx.y % a.hkv;
   const int rb = blockIdx.y / a.hkv;
   const int s = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, col = lane & 31;
+
+  // This lane's query row, and its query loads: they need only the launch
+  // shape (rows past the sequence's nodes still lie inside q and are zeroed
+  // below), so they go out together with the loads of the sequence's sizes,
+  // as does each thread's parent entry for the tree.
+  const int R = rb * a.rows_per_wg + wave * 32 + col;
+  const bool r_in = R < a.n_max * a.group;
+  bf16x8 qreg[kKSteps];
+  {
+    const int qn = r_in ? R / a.group : 0;
+    const int qh = hk * a.group + (r_in ? R % a.group : 0);
+    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                           (((int64_t)b * a.n_max + qn) * a.hq + qh) * D;
+#pragma unroll
+    for (int kk = 0; kk < kKSteps; ++kk) {
+      Pack8 p;
+      p.u = r_in ? *reinterpret_cast<const uint4*>(qrow + kk * 16 + half * 8)
+                 : make_uint4(0, 0, 0, 0);
+      qreg[kk] = p.v;
+    }
+  }
+  const int my_parent = tid < a.n_max ? a.parent[(int64_t)b * a.n_max + tid] : -1;
+
   // The sequence's sizes and cache offset are independent loads: one round
   // trip. The empty asm keeps the compiler from sinking the offset's load
   // below the early exits (a second round trip).
@@ -389,8 +437,6 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 
   const int begin = s * a.tps;
   const int end = (s == S - 1) ? T : begin + a.tps;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int half = lane >> 5, col = lane & 31;
 
   // Buffer resources over this sequence's K and V rows (all kv-heads).
   const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
@@ -434,25 +480,10 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 #pragma unroll
   for (int i = 0; i < NBUF - 1; ++i) dma_tile(i, begin + i * kTile);
 
-  // This lane's query row.
-  const int R = rb * a.rows_per_wg + wave * 32 + col;
   const bool row_ok = R < rows;
   const int n = row_ok ? R / a.group : 0;
   const int head = hk * a.group + (row_ok ? R % a.group : 0);
   const bool wave_active = rb * a.rows_per_wg + wave * 32 < rows;
-
-  bf16x8 qreg[kKSteps];
-  {
-    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
-                           (((int64_t)b * a.n_max + n) * a.hq + head) * D;
-#pragma unroll
-    for (int kk = 0; kk < kKSteps; ++kk) {
-      Pack8 p;
-      p.u = row_ok ? *reinterpret_cast<const uint4*>(qrow + kk * 16 + half * 8)
-                   : make_uint4(0, 0, 0, 0);
-      qreg[kk] = p.v;
-    }
-  }
 
   // LDS byte offsets used by this lane, independent of the tile.
   // K rows blk*32 + col, logical chunk 2*kk + half.
@@ -475,7 +506,7 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
   // split always does, and it reports the tree's status. With a malformed
   // tree the other splits still run; the sequence's output is unspecified.
   if (end > L) {
-    const bool ok = build_tree(a, b, N, s_parent, s_anc, &s_bad);
+    const bool ok = build_tree_loaded(N, my_parent, s_parent, s_anc, &s_bad);
     report_tree(a, b, ok, s == S - 1 && hk == 0 && rb == 0);
     if (!ok) {
       __builtin_amdgcn_s_waitcnt(0);      // no DMA may land after the workgroup ends
@@ -495,6 +526,10 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
   // Queries and the first tiles have landed. (This also tells the compiler
   // that no load it issued is pending, so it adds no waits inside the loop.)
   __builtin_amdgcn_s_waitcnt(0);
+  if (!row_ok) {
+#pragma unroll
+    for (int kk = 0; kk < kKSteps; ++kk) qreg[kk] = bf16x8{};
+  }
   for (int t0 = begin, buf = 0; t0 < end; t0 += kTile, buf = buf + 1 == NBUF ? 0 : buf + 1) {
     __builtin_amdgcn_s_waitcnt(kVmWait);  // this wave's DMA into `buf` has landed
     __syncthreads();                      // everyone's has; the previous buffer is free
