@@ -85,8 +85,7 @@ __global__ __launch_bounds__(kThreads) void accept_kernel(Args a) {
     }
     if (ok) key = (depth << 8) | (kThreads - 1 - n);   // larger depth, then lower index
   }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) key = max(key, shfl_xor(key, m));
+  key = wave_max(key);
   if ((n & (kWave - 1)) == 0) s_key[n / kWave] = key;
   __syncthreads();
   int top = s_key[0];

@@ -31,8 +31,77 @@ CURE_DEV uint32_t pack_bf16x2(float lo, float hi) {
 // exp2 on the hardware transcendental unit (v_exp_f32).
 CURE_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <typename T>
-CURE_DEV T shfl_xor(T v, int mask) { return __shfl_xor(v, mask, kWave); }
+CURE_DEV int lane_id() { return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
+
+// Butterfly partners for wave-wide reductions, on the VALU (DPP and lane
+// permutes) instead of the LDS crossbar. Stage k pairs each lane with a lane
+// whose group of k lanes is disjoint from its own:
+//   1, 2   quad permutes (lane ^ 1, lane ^ 2)
+//   4      half-row mirror (lane i <-> 7 - i within 8)
+//   8      row mirror (lane i <-> 15 - i within 16)
+//   16     swizzle, lane ^ 16 within 32
+//   32     permlane32 swap, lane ^ 32
+// Stages 4 and 8 are not xor patterns: they pair whole groups only once the
+// stages below them have run, so they are used only in the full sequence
+// 1, 2, 4, 8, 16, 32; stages 16 and 32 are true xors and may be used alone.
+// After a full sequence with a commutative merge every lane holds the same
+// wave-wide result.
+template <int kStage>
+CURE_DEV int partner(int v);
+template <>
+CURE_DEV int partner<1>(int v) { return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false); }
+template <>
+CURE_DEV int partner<2>(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false); }
+template <>
+CURE_DEV int partner<4>(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false); }
+template <>
+CURE_DEV int partner<8>(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false); }
+template <>
+CURE_DEV int partner<16>(int v) { return __builtin_amdgcn_ds_swizzle(v, 0x401F); }
+template <>
+CURE_DEV int partner<32>(int v) {
+  // Lanes 0-31 of the first result repeat lanes 0-31 of v; lanes 0-31 of the
+  // second hold lanes 32-63 of v (and the reverse for the upper half).
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)v, (unsigned)v, false, false);
+  return (int)(lane_id() < 32 ? r[1] : r[0]);
+}
+template <int kStage>
+CURE_DEV float partner(float v) { return __int_as_float(partner<kStage>(__float_as_int(v))); }
+
+// Sum and maximum of a value over lanes l and l ^ 32 (both halves get it).
+CURE_DEV float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+CURE_DEV float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+CURE_DEV float wave_max(float x) {
+  x = fmaxf(x, partner<1>(x));
+  x = fmaxf(x, partner<2>(x));
+  x = fmaxf(x, partner<4>(x));
+  x = fmaxf(x, partner<8>(x));
+  x = fmaxf(x, partner<16>(x));
+  return max_halves(x);
+}
+CURE_DEV int wave_max(int x) {
+  x = max(x, partner<1>(x));
+  x = max(x, partner<2>(x));
+  x = max(x, partner<4>(x));
+  x = max(x, partner<8>(x));
+  x = max(x, partner<16>(x));
+  return max(x, partner<32>(x));
+}
+CURE_DEV float wave_sum(float x) {
+  x += partner<1>(x);
+  x += partner<2>(x);
+  x += partner<4>(x);
+  x += partner<8>(x);
+  x += partner<16>(x);
+  return sum_halves(x);
+}
 
 // Top-2 under the order (value descending, index ascending). Empty slots hold
 // (-inf, INT32_MAX), which every real entry -- even -inf -- beats.
@@ -68,15 +137,20 @@ CURE_DEV Top2 top2_merge(const Top2& a, const Top2& b) {
   return {w1, lw ? l1 : w2, wi1, lw ? li1 : wi2};
 }
 
+template <int kStage>
+CURE_DEV Top2 top2_stage(const Top2& t) {
+  const Top2 o{partner<kStage>(t.v1), partner<kStage>(t.v2), partner<kStage>(t.i1),
+               partner<kStage>(t.i2)};
+  return top2_merge(t, o);
+}
+
 CURE_DEV Top2 top2_wave_reduce(Top2 t) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    Top2 o;
-    o.v1 = shfl_xor(t.v1, m); o.i1 = shfl_xor(t.i1, m);
-    o.v2 = shfl_xor(t.v2, m); o.i2 = shfl_xor(t.i2, m);
-    t = top2_merge(t, o);
-  }
-  return t;
+  t = top2_stage<1>(t);
+  t = top2_stage<2>(t);
+  t = top2_stage<4>(t);
+  t = top2_stage<8>(t);
+  t = top2_stage<16>(t);
+  return top2_stage<32>(t);
 }
 
 // Log-sum-exp state: the sum of exp(x - ref) over the entries seen, with a
@@ -92,13 +166,18 @@ CURE_DEV Lse lse_merge(Lse a, Lse b) {
   return {r, a.sum * fast_exp2((a.ref - r) * kLog2e) + b.sum * fast_exp2((b.ref - r) * kLog2e)};
 }
 
+template <int kStage>
+CURE_DEV Lse lse_stage(const Lse& s) {
+  return lse_merge(s, Lse{partner<kStage>(s.ref), partner<kStage>(s.sum)});
+}
+
 CURE_DEV Lse lse_wave_reduce(Lse s) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    Lse o{shfl_xor(s.ref, m), shfl_xor(s.sum, m)};
-    s = lse_merge(s, o);
-  }
-  return s;
+  s = lse_stage<1>(s);
+  s = lse_stage<2>(s);
+  s = lse_stage<4>(s);
+  s = lse_stage<8>(s);
+  s = lse_stage<16>(s);
+  return lse_stage<32>(s);
 }
 
 CURE_DEV float lse_value(Lse s) {

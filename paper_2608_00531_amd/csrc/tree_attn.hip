@@ -238,14 +238,12 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
       const bool vis = tok < end && visible(tok, L, N, n, s_anc);
       const float x = vis ? sc[i] * a.scale_log2 : -INFINITY;
       float mt = x;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) mt = fmaxf(mt, shfl_xor(mt, m));
+      mt = wave_max(mt);
       const float m_new = fmaxf(m_run[i], mt);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       const float p = exp2f(x - m_use);
       float ps = p;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) ps += shfl_xor(ps, m);
+      ps = wave_sum(ps);
       const float alpha = exp2f(m_run[i] - m_use);
       l_run[i] = l_run[i] * alpha + ps;
       m_run[i] = m_new;
@@ -576,7 +574,7 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
       for (int r = 0; r < 16; r += 2) mloc = fmaxf(mloc, fmaxf(sacc[blk][r], sacc[blk][r + 1]));
-    const float m_tile = fmaxf(mloc, shfl_xor(mloc, 32)) * c;
+    const float m_tile = max_halves(mloc) * c;
     // Lazy rescale: move the reference only when the maximum rises by > 2^8.
     const bool grow = m_tile > m_run + kRescaleLog2;
     if (__builtin_expect(__ballot(grow) != 0, 0)) {
@@ -629,7 +627,7 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 
   __builtin_amdgcn_s_waitcnt(0);          // the ring's trailing DMAs land before exit
   if (!row_ok) return;
-  const float l_tot = l_run + shfl_xor(l_run, 32);
+  const float l_tot = sum_halves(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_nat = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
   if (S == 1) {
@@ -714,8 +712,7 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   load_batch(0);
   float m = -INFINITY;
   for (int sp = lane; sp < S; sp += kWave) m = fmaxf(m, a.part_lse[p0 + sp]);
-#pragma unroll
-  for (int k = 32; k >= 1; k >>= 1) m = fmaxf(m, shfl_xor(m, k));
+  m = wave_max(m);
   const float ms = m == -INFINITY ? 0.f : m;     // empty splits (lse = -inf) weigh 0
 
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -734,14 +731,18 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
     if (s0 >= S) break;
     load_batch(s0);
   }
-#pragma unroll
-  for (int k = kLanesPerSplit; k < kWave; k <<= 1) {
-    acc.x += shfl_xor(acc.x, k);
-    acc.y += shfl_xor(acc.y, k);
-    acc.z += shfl_xor(acc.z, k);
-    acc.w += shfl_xor(acc.w, k);
-    wsum += shfl_xor(wsum, k);
+  if (kLanesPerSplit == 16) {                       // lane groups 16 apart
+    acc.x += partner<16>(acc.x);
+    acc.y += partner<16>(acc.y);
+    acc.z += partner<16>(acc.z);
+    acc.w += partner<16>(acc.w);
+    wsum += partner<16>(wsum);
   }
+  acc.x = sum_halves(acc.x);                        // and 32 apart
+  acc.y = sum_halves(acc.y);
+  acc.z = sum_halves(acc.z);
+  acc.w = sum_halves(acc.w);
+  wsum = sum_halves(wsum);
   if (sub != 0) return;
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D + col;
