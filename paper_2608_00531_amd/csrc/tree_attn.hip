@@ -342,6 +342,15 @@ union Pack8 {
 };
 
 constexpr int kRsrcWord3 = 0x00020000;     // raw (untyped) 32-bit access, gfx9 family
+
+// Three-input maximum as one v_max3_f32. Written as assembly because fmaxf
+// first canonicalises every operand that may be a signalling NaN (an extra
+// instruction per score); scores here are finite dot products or -inf.
+CURE_DEV float max3_raw(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
 constexpr float kRescaleLog2 = 8.f;       // lazy rescale threshold (log2 units)
 
 template <int D>
@@ -569,12 +578,13 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
           if (!(tok < end && visible(tok, L, N, n, s_anc))) sacc[blk][r] = -INFINITY;
         }
     }
-    float mloc = -INFINITY;
+    // Row maximum: one three-input max per two scores, in two chains.
+    float mb[2] = {-INFINITY, -INFINITY};
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) mloc = fmaxf(mloc, fmaxf(sacc[blk][r], sacc[blk][r + 1]));
-    const float m_tile = max_halves(mloc) * c;
+      for (int r = 0; r < 16; r += 2) mb[blk] = max3_raw(mb[blk], sacc[blk][r], sacc[blk][r + 1]);
+    const float m_tile = max_halves(max3_raw(mb[0], mb[1], mb[1])) * c;
     // Lazy rescale: move the reference only when the maximum rises by > 2^8.
     const bool grow = m_tile > m_run + kRescaleLog2;
     if (__builtin_expect(__ballot(grow) != 0, 0)) {
