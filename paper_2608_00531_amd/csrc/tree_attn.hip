@@ -307,6 +307,7 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -676,6 +677,266 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 }
 
 // ---------------------------------------------------------------------------
+// MFMA split kernel with 16 query rows per wave (v_mfma_f32_16x16x32_bf16).
+//
+// Same tile stream, LDS layout, tree mask and online softmax as the 32-row
+// kernel above, at half the registers per wave, so that two 8-wave
+// workgroups (four waves per SIMD) share a CU and larger row counts (up to
+// 256) fit one workgroup with the rows spread evenly over the SIMDs.
+//
+// Lane l = 16 g + c (c = l % 16, g = l / 16) owns query row c of its wave.
+//   S^T = K Q^T, per 16-token block tb and 32-wide k-step ks:
+//     A = K rows tb*16 + c, columns 32 ks + 8 g .. +7   (one 16-byte LDS read)
+//     B = Q row c, columns 32 ks + 8 g .. +7             (registers)
+//     D register r = score of token tb*16 + 4 g + r for row c
+//   so a row's 64 scores sit in the four lanes c, c+16, c+32, c+48 and its
+//   statistics reduce over lane xor 16 and xor 32.
+//   O^T += V^T P^T, per 16-wide column block db and 32-token k-step kt, with
+//   the k index 8 g + j standing for token 32 kt + 4 g + j (j < 4) or
+//   32 kt + 16 + 4 g + (j - 4) (j >= 4): exactly the probabilities lane l
+//   already holds from blocks 2 kt and 2 kt + 1, so P needs no exchange.
+//     A = V^T: two transposed reads of 4 tokens x 16 columns per 16 lanes
+//     D register r = O column 16 db + 4 g + r of row c
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a) {
+  using G = TileGeo<D>;
+  constexpr int kKSteps = D / 32;                  // k-steps for Q K^T
+  constexpr int kDBlk = D / 16;                    // 16-column blocks of O^T
+  constexpr int kDmaPerWave = G::kBlocks / NW;     // DMA blocks per wave per tensor
+  static_assert(G::kBlocks % NW == 0, "tile must split evenly across waves");
+
+  __shared__ int s_parent[CURE_MAX_TREE_NODES];
+  __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
+  __shared__ int s_bad;
+  __shared__ __attribute__((aligned(1024))) unsigned char s_k[2][G::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_v[2][G::kTileBytes];
+
+  const int b = blockIdx.z;
+  const int hk = blockIdx.y % a.hkv;
+  const int rb = blockIdx.y / a.hkv;
+  const int s = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane & 15, g = lane >> 4;
+
+  // Query loads (need only the launch shape) and the parent entry go out with
+  // the loads of the sequence's sizes.
+  const int R = rb * a.rows_per_wg + wave * 16 + c;
+  const bool r_in = R < a.n_max * a.group;
+  bf16x8 qreg[kKSteps];
+  {
+    const int qn = r_in ? R / a.group : 0;
+    const int qh = hk * a.group + (r_in ? R % a.group : 0);
+    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                           (((int64_t)b * a.n_max + qn) * a.hq + qh) * D;
+#pragma unroll
+    for (int ks = 0; ks < kKSteps; ++ks) {
+      Pack8 p;
+      p.u = r_in ? *reinterpret_cast<const uint4*>(qrow + ks * 32 + g * 8)
+                 : make_uint4(0, 0, 0, 0);
+      qreg[ks] = p.v;
+    }
+  }
+  const int my_parent = tid < a.n_max ? a.parent[(int64_t)b * a.n_max + tid] : -1;
+
+  const int n_raw = a.n_nodes[b];
+  const int L = a.ctx_len[b];
+  const int64_t off = a.kv_off[b];
+  asm volatile("" : : "s"(n_raw), "s"(L), "s"(off));
+  const int N = min(n_raw, a.n_max);
+  const int T = L + N;
+  const int S = split_count(T, N, a.tps, a.max_splits);
+  const int rows = N * a.group;
+  if (S == 0) {                         // no nodes: nothing to compute; the empty tree is valid
+    report_tree(a, b, true, s == 0 && hk == 0 && rb == 0);
+    return;
+  }
+  if (s >= S || rb * a.rows_per_wg >= rows) return;
+
+  const int begin = s * a.tps;
+  const int end = (s == S - 1) ? T : begin + a.tps;
+
+  const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.k)) + off * a.hkv * D, 0,
+      (int)seq_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.v)) + off * a.hkv * D, 0,
+      (int)seq_bytes, kRsrcWord3);
+  uint32_t src_off[kDmaPerWave];
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int byte = (wave * kDmaPerWave + j) * 1024 + lane * 16;
+    const int row = byte / G::kRowBytes;
+    const int pchunk = (byte % G::kRowBytes) >> 4;
+    const int lchunk = pchunk ^ G::swz(row);
+    src_off[j] = (uint32_t)((row * a.hkv + hk) * G::kRowBytes + (lchunk << 4));
+  }
+  const uint32_t tok_bytes = (uint32_t)(a.hkv * G::kRowBytes);
+  const i32x4 rk4 = as_i32x4(rk), rv4 = as_i32x4(rv);
+  auto dma_tile = [&](int buf, int t0) {
+    const bool live = t0 < end;
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) {
+      const uint32_t voff = live ? src_off[j] + (uint32_t)t0 * tok_bytes : kOobOffset;
+      const int blk = (wave * kDmaPerWave + j) * 1024;
+      dma16(lds_addr(&s_k[buf][blk]), voff, rk4);
+      dma16(lds_addr(&s_v[buf][blk]), voff, rv4);
+    }
+  };
+  dma_tile(0, begin);
+
+  const bool row_ok = R < rows;
+  const int n = row_ok ? R / a.group : 0;
+  const int head = hk * a.group + (row_ok ? R % a.group : 0);
+  const bool wave_active = rb * a.rows_per_wg + wave * 16 < rows;
+
+  // LDS byte offsets of this lane's operands inside a tile.
+  int k_off[4][kKSteps];                           // K: row tb*16 + c, chunk 4 ks + g
+#pragma unroll
+  for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+    for (int ks = 0; ks < kKSteps; ++ks) k_off[tb][ks] = G::offset(tb * 16 + c, 4 * ks + g);
+  // V: within a 16-lane group, lane j = c addresses row 4 g + j / 4 (+16) of
+  // the k-step's 32 tokens, columns 16 db + 4 (j % 4) .. +3.
+  const int v_row = 4 * g + (c >> 2);
+  const int v_chunk = (c & 3) >> 1;                // + 2 db
+  const int v_byte = (c & 1) * 8;
+
+  if (end > L) {
+    const bool ok = build_tree_loaded(N, my_parent, s_parent, s_anc, &s_bad);
+    report_tree(a, b, ok, s == S - 1 && hk == 0 && rb == 0);
+    if (!ok) {
+      __builtin_amdgcn_s_waitcnt(0);
+      return;
+    }
+  }
+
+  f32x4 oacc[kDBlk];
+#pragma unroll
+  for (int i = 0; i < kDBlk; ++i) oacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;            // l_run: this lane's share of the row sum
+  const float cs = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  __builtin_amdgcn_s_waitcnt(0);
+  if (!row_ok) {
+#pragma unroll
+    for (int ks = 0; ks < kKSteps; ++ks) qreg[ks] = bf16x8{};
+  }
+  for (int t0 = begin, buf = 0; t0 < end; t0 += kTile, buf ^= 1) {
+    __builtin_amdgcn_s_waitcnt(0);        // this wave's DMA into `buf` has landed
+    __syncthreads();                      // everyone's has; the other buffer is free
+    dma_tile(buf ^ 1, t0 + kTile);
+    if (!wave_active) continue;
+    const unsigned char* kt = s_k[buf];
+    const unsigned char* vt = s_v[buf];
+
+    // Scores: four 16-token blocks, each a chain of kKSteps MFMAs.
+    f32x4 sacc[4];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) sacc[tb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < kKSteps; ++ks)
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        Pack8 ka;
+        ka.u = *reinterpret_cast<const uint4*>(kt + k_off[tb][ks]);
+        sacc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka.v, qreg[ks], sacc[tb], 0, 0, 0);
+      }
+    if (t0 + kTile > L) {
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tok = t0 + tb * 16 + 4 * g + r;
+          if (!(tok < end && visible(tok, L, N, n, s_anc))) sacc[tb][r] = -INFINITY;
+        }
+    }
+    // Row maximum over the lane's 16 scores (eight v_max3), then its 3 partners.
+    float mb = max3_raw(sacc[0][0], sacc[0][1], sacc[0][2]);
+#pragma unroll
+    for (int i = 3; i < 15; i += 2)
+      mb = max3_raw(mb, sacc[i >> 2][i & 3], sacc[(i + 1) >> 2][(i + 1) & 3]);
+    mb = max3_raw(mb, sacc[3][3], sacc[3][3]);
+    mb = max3_raw(mb, partner<16>(mb), mb);
+    const float m_tile = max_halves(mb) * cs;
+    const bool grow = m_tile > m_run + kRescaleLog2;
+    if (__builtin_expect(__ballot(grow) != 0, 0)) {
+      if (grow) {
+        const float alpha = fast_exp2(m_run - m_tile);
+        l_run *= alpha;
+#pragma unroll
+        for (int i = 0; i < kDBlk; ++i) oacc[i] *= alpha;
+        m_run = m_tile;
+      }
+    }
+    const float nm = m_run == -INFINITY ? 0.f : -m_run;
+    bf16x8 pb[2];                                  // k-steps kt = 0, 1 (blocks 2 kt, 2 kt + 1)
+    float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2) {
+      bf16x8 v8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        v8[j] = (__bf16)fast_exp2(fmaf(sacc[2 * kt2 + (j >> 2)][j & 3], cs, nm));
+      pb[kt2] = v8;
+      l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
+      l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
+      l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
+      l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+    }
+    l_run += l0 + l1;
+
+#pragma unroll
+    for (int kt2 = 0; kt2 < 2; ++kt2)
+#pragma unroll
+      for (int db = 0; db < kDBlk; ++db) {
+        Pack8 va;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 32 * kt2 + 16 * h + v_row;
+          const int byte = G::offset(row, 2 * db + v_chunk) + v_byte;
+          va.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vt + byte));
+        }
+        oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va.v, pb[kt2], oacc[db], 0, 0, 0);
+      }
+  }
+
+  __builtin_amdgcn_s_waitcnt(0);          // the trailing out-of-range DMA lands before exit
+  if (!row_ok) return;
+  float l_tot = l_run + partner<16>(l_run);
+  l_tot = sum_halves(l_tot);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse_nat = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
+  if (S == 1) {
+    const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+    for (int db = 0; db < kDBlk; ++db) {
+      const int d0 = db * 16 + 4 * g;
+      const float x0 = oacc[db][0] * inv, x1 = oacc[db][1] * inv;
+      const float x2 = oacc[db][2] * inv, x3 = oacc[db][3] * inv;
+      if (a.out_bf16) {
+        uint2 pk;
+        pk.x = pack_bf16x2(x0, x1);
+        pk.y = pack_bf16x2(x2, x3);
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.o) + obase + d0) = pk;
+      } else {
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.o) + obase + d0) =
+            make_float4(x0, x1, x2, x3);
+      }
+    }
+    if (g == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] = lse_nat;
+  } else {
+    const int64_t pi = part_index(a, b, head, n, s);
+#pragma unroll
+    for (int db = 0; db < kDBlk; ++db)
+      *reinterpret_cast<float4*>(a.part_o + pi * D + db * 16 + 4 * g) =
+          make_float4(oacc[db][0] * inv, oacc[db][1] * inv, oacc[db][2] * inv, oacc[db][3] * inv);
+    if (g == 0) a.part_lse[pi] = lse_nat;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // LSE merge: one wave per output row (b, n, head).
 //
 // A split's partial row is D floats = D/4 lanes of float4, so one load
@@ -768,6 +1029,7 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
 // Host-side plan: tokens per split and the launch shape.
 struct Plan {
   bool mfma;
+  bool rows16;        // MFMA kernel with 16 query rows per wave
   int nw;             // waves per workgroup (MFMA kernel)
   int rows_per_wg;
   int row_blocks;
@@ -778,12 +1040,14 @@ struct Plan {
 // MFMA workgroups one CU holds at once: bounded by LDS (the K/V ring plus the
 // tree masks) and by registers (about 220 VGPRs per lane at head dim 128, so
 // two waves per SIMD; about 120 at head dim 64, four waves per SIMD).
-int mfma_wgs_per_cu(int d, int nw) {
+int mfma_wgs_per_cu(int d, int nw, bool rows16) {
   constexpr int kLdsPerCu = 160 * 1024;
-  const int lds = 2 * kStages * kTile * d * 2 +
+  const int stages = rows16 ? 2 : kStages;
+  const int lds = 2 * stages * kTile * d * 2 +
                   CURE_MAX_TREE_NODES * (4 + kAncWords * 8) + 64;
   const int by_lds = kLdsPerCu / lds;
-  const int by_regs = (d == 128 ? 8 : 16) / nw;
+  // 16-row waves hold about half the registers: four waves per SIMD.
+  const int by_regs = rows16 ? 16 / nw : (d == 128 ? 8 : 16) / nw;
   return std::max(1, std::min(by_lds, by_regs));
 }
 
@@ -794,14 +1058,24 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   p.mfma = mfma;
   const int group = hq / hkv;
   const int rows = n_max * group;
-  if (mfma) {
-    p.nw = rows <= 128 ? 4 : 8;
-    p.rows_per_wg = 32 * p.nw;
+  // Up to 256 rows per kv-head (128 at head dim 64) the 16-row kernel takes
+  // them in one workgroup: 8 waves for up to 128 rows, else 16. Beyond that
+  // the 32-row kernel's 8-wave row blocks (256 rows each) measured faster.
+  p.rows16 = mfma && rows <= (d == 128 ? 256 : 128);
+  if (p.rows16) {
+    p.nw = rows > 128 ? 16 : 8;
+    p.row_blocks = 1;
+    p.rows_per_wg = 16 * p.nw;
   } else {
-    p.nw = kValuWaves;
-    p.rows_per_wg = kValuRows;
+    if (mfma) {
+      p.nw = rows <= 128 ? 4 : 8;
+      p.rows_per_wg = 32 * p.nw;
+    } else {
+      p.nw = kValuWaves;
+      p.rows_per_wg = kValuRows;
+    }
+    p.row_blocks = std::max(1, (rows + p.rows_per_wg - 1) / p.rows_per_wg);
   }
-  p.row_blocks = std::max(1, (rows + p.rows_per_wg - 1) / p.rows_per_wg);
   int64_t t_max = 0, t_sum = 0;
   for (int b = 0; b < batch; ++b) {
     const int N = std::min(host_n_nodes[b], n_max);
@@ -829,7 +1103,7 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
     // The shortest split (at least kMinTps tokens) whose workgroups are all
     // resident at once, so no workgroup waits for a second round. A batch with
     // more sequence x head pairs than that gets a single split per sequence.
-    const int64_t slots = (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw) : 2) * device_cu_count();
+    const int64_t slots = (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw, p.rows16) : 2) * device_cu_count();
     const int64_t hi = round_tile(t_max);
     int64_t lo = round_tile(std::max<int64_t>(
         kMinTps, (t_sum * hkv * p.row_blocks + slots - 1) / std::max<int64_t>(1, slots)));
@@ -955,7 +1229,14 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
 
   hipStream_t st = as_stream(stream);
   const dim3 grid(p.max_splits, hkv * p.row_blocks, batch);
-  if (mfma) {
+  if (p.rows16) {
+    if (d == 128) {
+      if (p.nw == 8) hipLaunchKernelGGL((tree_attn_m16<128, 8>), grid, dim3(512), 0, st, a);
+      else hipLaunchKernelGGL((tree_attn_m16<128, 16>), grid, dim3(1024), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((tree_attn_m16<64, 8>), grid, dim3(512), 0, st, a);
+    }
+  } else if (mfma) {
     if (d == 128) {
       if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<128, 4, kStages>), grid, dim3(256), 0, st, a);
       else hipLaunchKernelGGL((tree_attn_mfma<128, 8, kStages>), grid, dim3(512), 0, st, a);
