@@ -297,6 +297,7 @@ def main():
         calls = per_call_times(torch, steps, min(args.steps, 100))
     status = steps[0].status.cpu().tolist()
     assert status == [0] * w.batch, status
+    acc_len = steps[0].acc["acc_len"].float().cpu()
 
     call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"]}
     kernels = {}
@@ -307,7 +308,7 @@ def main():
     dom = max(calls, key=calls.get)
     dom_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
     names = {"margins": "cure_margins (margins_kernel)",
-             "attn": "cure_tree_attn (tree_attn_mfma + attn_merge)",
+             "attn": "cure_tree_attn (tree_attn_m16 or tree_attn_mfma, + attn_merge)",
              "accept": "cure_accept (accept_kernel)"}
     value = step_bytes / (ms * 1e-3) / 1e9
     line = {
@@ -331,6 +332,8 @@ def main():
         "kv_gbps": round(ab["attention_kv"] / (calls["attn"] * 1e-6) / 1e9, 1),
         "event_ms_per_step": round(ev_ms, 5),
         "kernels": kernels,
+        # Mean accepted draft length of the step's sequences (tokens emitted = +1).
+        "acc_len_mean": round(float(acc_len.mean()), 3),
         "roofline": {"bound": "hbm", "kernel": names[dom], "achieved": round(dom_gbs, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
