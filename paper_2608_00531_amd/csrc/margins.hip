@@ -300,34 +300,51 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
 // Per sequence: merge each row's chunk results (when rows were split), then
 // select the sequence's UFPs from its chain rows' margins.
 //
-// One thread per row. A row's chunk results are contiguous; a thread issues
-// the loads of kFinishBatch of them before merging any, so a row with up to
-// kFinishBatch chunks costs one memory round trip. The chain rows' margins go
-// to LDS as they are produced, so the gate needs no second trip to memory.
-constexpr int kFinishBatch = 16;
+// Eight lanes per row: lane k of a row's group loads chunk results k, k + 8,
+// k + 16, k + 24 (all at once, one memory round trip), merges them, and the
+// group combines its eight results through VALU lane exchanges. The chain
+// rows' margins go to LDS as they are produced, so the gate needs no second
+// trip to memory.
+constexpr int kFinishGroup = 8;
+constexpr int kFinishPerLane = kMaxSplits / kFinishGroup;
+static_assert(kMaxSplits % kFinishGroup == 0, "chunk results split evenly over a row's lanes");
 
 __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
   __shared__ float s_margin[kMaxGateChain];
   const int b = blockIdx.x;
   if (a.splits > 1) {
-    for (int r = threadIdx.x; r < a.rows; r += kThreads) {
-      const Partial* p = a.partials + ((int64_t)b * a.rows + r) * a.splits;
-      Top2 t = top2_empty();
-      Lse ls{kLseEmptyRef, 0.f};
-      for (int s0 = 0; s0 < a.splits; s0 += kFinishBatch) {
-        Partial q[kFinishBatch];
+    constexpr int kRowsPerPass = kThreads / kFinishGroup;
+    const int k = threadIdx.x % kFinishGroup;
+    // Every lane runs the same number of passes: the lane exchanges below
+    // need all eight lanes of a group active.
+    for (int r0 = 0; r0 < a.rows; r0 += kRowsPerPass) {
+      const int r = r0 + threadIdx.x / kFinishGroup;
+      const bool live = r < a.rows;
+      const Partial* p = a.partials + ((int64_t)b * a.rows + (live ? r : 0)) * a.splits;
+      Partial q[kFinishPerLane];
 #pragma unroll
-        for (int u = 0; u < kFinishBatch; ++u)
-          if (s0 + u < a.splits) q[u] = p[s0 + u];
-#pragma unroll
-        for (int u = 0; u < kFinishBatch; ++u)
-          if (s0 + u < a.splits) {
-            t = top2_merge(t, Top2{q[u].v1, q[u].v2, q[u].i1, q[u].i2});
-            ls = lse_merge(ls, Lse{q[u].ref, q[u].sum});
-          }
+      for (int u = 0; u < kFinishPerLane; ++u) {
+        const int sp = k + u * kFinishGroup;
+        q[u] = Partial{kLseEmptyRef, 0.f, -INFINITY, -INFINITY, INT32_MAX, INT32_MAX, 0, 0};
+        if (live && sp < a.splits) q[u] = p[sp];
       }
-      write_row(a, b * a.rows + r, t, lse_value(ls));
-      if (r < a.chain_len) s_margin[r] = t.v1 - t.v2;
+      Top2 t{q[0].v1, q[0].v2, q[0].i1, q[0].i2};
+      Lse ls{q[0].ref, q[0].sum};
+#pragma unroll
+      for (int u = 1; u < kFinishPerLane; ++u) {
+        t = top2_merge(t, Top2{q[u].v1, q[u].v2, q[u].i1, q[u].i2});
+        ls = lse_merge(ls, Lse{q[u].ref, q[u].sum});
+      }
+      t = top2_stage<1>(t);
+      t = top2_stage<2>(t);
+      t = top2_stage<4>(t);
+      ls = lse_stage<1>(ls);
+      ls = lse_stage<2>(ls);
+      ls = lse_stage<4>(ls);
+      if (live && k == 0) {
+        write_row(a, b * a.rows + r, t, lse_value(ls));
+        if (r < a.chain_len) s_margin[r] = t.v1 - t.v2;
+      }
     }
   } else if (a.ufp_pos) {
     for (int i = threadIdx.x; i < a.chain_len; i += kThreads)

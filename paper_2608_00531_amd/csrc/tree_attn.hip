@@ -958,31 +958,48 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   const int head = (int)(rowid % a.hq);
   const int n = (int)((rowid / a.hq) % a.n_max);
   const int b = (int)(rowid / ((int64_t)a.hq * a.n_max));
+  const int64_t p0 = part_index(a, b, head, n, 0);
+  const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
+  const int col = (lane % kLanesPerSplit) * 4;      // its four output columns
+
+  // The first batch of partials is loaded together with the sequence's sizes
+  // (its addresses need neither): one memory round trip. Slots past the
+  // sequence's own split count hold stale data and are masked out below.
+  float4 v[NB];
+  float l[NB];
+  auto load_batch = [&](int s0, int limit) {
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int sp = s0 + u * kSplitsPerLoad + sub;
+      const bool ok = sp < limit;
+      v[u] = ok ? *reinterpret_cast<const float4*>(a.part_o + (p0 + sp) * D + col)
+                : make_float4(0.f, 0.f, 0.f, 0.f);
+      l[u] = ok ? a.part_lse[p0 + sp] : -INFINITY;
+    }
+  };
+  load_batch(0, a.max_splits);
   const int n_raw = a.n_nodes[b];
   const int L = a.ctx_len[b];
   const int N = min(n_raw, a.n_max);
   if (n >= N) return;
   const int S = split_count(L + N, N, a.tps, a.max_splits);
   if (S <= 1) return;
-  const int64_t p0 = part_index(a, b, head, n, 0);
-  const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
-  const int col = (lane % kLanesPerSplit) * 4;      // its four output columns
-
-  float4 v[NB];
-  float l[NB];
-  auto load_batch = [&](int s0) {
 #pragma unroll
-    for (int u = 0; u < NB; ++u) {
-      const int sp = s0 + u * kSplitsPerLoad + sub;
-      const bool ok = sp < S;
-      v[u] = ok ? *reinterpret_cast<const float4*>(a.part_o + (p0 + sp) * D + col)
-                : make_float4(0.f, 0.f, 0.f, 0.f);
-      l[u] = ok ? a.part_lse[p0 + sp] : -INFINITY;
+  for (int u = 0; u < NB; ++u) {
+    if (u * kSplitsPerLoad + sub >= S) {
+      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      l[u] = -INFINITY;
     }
-  };
-  load_batch(0);
+  }
+  // Reference maximum: from the loaded batch when it holds every split, else
+  // from all of the row's LSEs.
   float m = -INFINITY;
-  for (int sp = lane; sp < S; sp += kWave) m = fmaxf(m, a.part_lse[p0 + sp]);
+  if (S <= kSplitsPerBatch) {
+#pragma unroll
+    for (int u = 0; u < NB; ++u) m = fmaxf(m, l[u]);
+  } else {
+    for (int sp = lane; sp < S; sp += kWave) m = fmaxf(m, a.part_lse[p0 + sp]);
+  }
   m = wave_max(m);
   const float ms = m == -INFINITY ? 0.f : m;     // empty splits (lse = -inf) weigh 0
 
@@ -1000,7 +1017,7 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
     }
     s0 += kSplitsPerBatch;
     if (s0 >= S) break;
-    load_batch(s0);
+    load_batch(s0, S);
   }
   if (kLanesPerSplit == 16) {                       // lane groups 16 apart
     acc.x += partner<16>(acc.x);
@@ -1068,7 +1085,7 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
     p.rows_per_wg = 16 * p.nw;
   } else {
     if (mfma) {
-      p.nw = rows <= 128 ? 4 : 8;
+      p.nw = 8;
       p.rows_per_wg = 32 * p.nw;
     } else {
       p.nw = kValuWaves;
@@ -1237,13 +1254,8 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
       hipLaunchKernelGGL((tree_attn_m16<64, 8>), grid, dim3(512), 0, st, a);
     }
   } else if (mfma) {
-    if (d == 128) {
-      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<128, 4, kStages>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((tree_attn_mfma<128, 8, kStages>), grid, dim3(512), 0, st, a);
-    } else {
-      if (p.nw == 4) hipLaunchKernelGGL((tree_attn_mfma<64, 4, kStages>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((tree_attn_mfma<64, 8, kStages>), grid, dim3(512), 0, st, a);
-    }
+    if (d == 128) hipLaunchKernelGGL((tree_attn_mfma<128, 8, kStages>), grid, dim3(512), 0, st, a);
+    else hipLaunchKernelGGL((tree_attn_mfma<64, 8, kStages>), grid, dim3(512), 0, st, a);
   } else {
     if (dtype == CURE_BF16) {
       if (d == 128) hipLaunchKernelGGL((tree_attn_valu<uint16_t, 128>), grid, dim3(256), 0, st, a);
