@@ -95,12 +95,18 @@ def test_ragged_nodes_and_contexts():
         check_attn(w, o, lse, ref_o, ref_l)
 
 
-@pytest.mark.parametrize("hq,hkv,n_ufp,depth", [(32, 8, 16, 4), (8, 8, 16, 15), (4, 1, 8, 4)])
-def test_row_blocking_and_wide_trees(hq, hkv, n_ufp, depth):
-    # (32,8,16,4): 80 nodes x G4 = 320 rows -> two row blocks of the 8-wave kernel;
-    # (8,8,16,15): 256 nodes (the maximum), G1; (4,1,8,4): 48 nodes x G4 = 192 rows.
-    say("attn rows", hq, hkv, n_ufp, depth)
-    w = make_workload("w", batch=1, hq=hq, hkv=hkv, ctx_lens=[777], chain_len=16,
+@pytest.mark.parametrize("hq,hkv,d,n_ufp,depth", [(32, 8, 128, 16, 4), (8, 8, 128, 16, 15),
+                                                  (4, 1, 128, 8, 4), (4, 1, 64, 8, 4),
+                                                  (32, 8, 128, 2, 4)])
+def test_row_blocking_and_wide_trees(hq, hkv, d, n_ufp, depth):
+    # Rows per kv-head = nodes x group:
+    # (32,8,128,16,4): 80 x 4 = 320 -> two row blocks of the 32-row kernel;
+    # (8,8,128,16,15): 256 nodes (the maximum), G1 -> 16-row kernel, 16 waves;
+    # (4,1,128,8,4): 48 x 4 = 192 -> 16-row kernel, 12 of 16 waves;
+    # (4,1,64,8,4): 192 rows at head dim 64 -> 32-row kernel;
+    # (32,8,128,2,4): 24 x 4 = 96 -> 16-row kernel, 6 of 8 waves.
+    say("attn rows", hq, hkv, d, n_ufp, depth)
+    w = make_workload("w", batch=1, hq=hq, hkv=hkv, d=d, ctx_lens=[777], chain_len=16,
                       n_ufp=n_ufp, branch_depth=depth, seed=90)
     dev = upload(w)
     for flags in (0, pc.CURE_ATTN_FORCE_VALU):
