@@ -22,6 +22,11 @@ unless the paper (or the decision being reproduced) fixes another precision:
                        its own ancestors.
 * ``accept``        -- accepted prefix length per path and the best path,
                        Sec. 3.1 Eq. (1) and Sec. 3.5 Eq. (4).
+* ``topk``, ``branch_budget``, ``repair_tree``
+                    -- the repair tree, Eq. (3), Algorithm 1 and Sec. 3.4:
+                       ranked alternatives by a full stable sort, the branch
+                       budget per UFP, and the budget-capped assembly of the
+                       parent/token arrays.
 
 Inputs are the same bytes the GPU path receives: bf16 arrives as raw uint16
 bit patterns and is widened here exactly to float32 by this package's own
@@ -31,8 +36,10 @@ code. Logit values must be finite or -inf.
 from .margins import widen_bf16, as_float32, margins, ufp_select
 from .tree import ancestors, tree_attention
 from .accept import accept
+from .repair import topk, branch_budget, repair_tree
 
 __all__ = [
     "widen_bf16", "as_float32", "margins", "ufp_select",
     "ancestors", "tree_attention", "accept",
+    "topk", "branch_budget", "repair_tree",
 ]
