@@ -2,7 +2,7 @@
  * libcure -- MI355X (gfx950) verify-and-repair hot path of CURE
  * (local uncertainty repair for block-parallel speculative decoding).
  *
- * Three stream-ordered entry points cover one decoding iteration's data-parallel
+ * Stream-ordered entry points cover one decoding iteration's data-parallel
  * work on the device:
  *
  *   cure_margins    top-1/top-2 margin and log-sum-exp per logits row, plus the
@@ -10,6 +10,9 @@
  *   cure_tree_attn  tree-masked verification attention over the KV cache and
  *                   each node's own tree ancestors           (Sec. 3.2, 3.4, 3.5)
  *   cure_accept     accepted prefix per path and the best path     (Eq. 1, Eq. 4)
+ *   cure_repair_tree  the budget-aware repair tree: ranked alternatives at the
+ *                   UFPs, the Eq. 3 branch budget and the parent/token arrays
+ *                                                       (Sec. 3.3, 3.4, Alg. 1)
  *
  * Conventions shared by every entry point
  *  - All array arguments are DEVICE pointers (memory the caller allocated with
@@ -171,6 +174,65 @@ cure_status cure_accept(const int32_t* parent, const int32_t* token, const int32
                         const int32_t* root_tgt, const int32_t* n_nodes, int32_t chain_len,
                         int32_t batch, int32_t n_max, int32_t* acc_len, int32_t* path,
                         int32_t* best, int32_t* bonus, int32_t* resync, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Repair-tree construction -- Sec. 3.3 Eq. (3), Sec. 3.4, Algorithm 1.
+ *
+ * Builds each sequence's candidate tree from its draft block (branch 0) and
+ * the UFPs that cure_margins selected. For UFP slot s (in the given,
+ * ascending-margin order) at block position u = ufp_pos[b][s]:
+ *   ranked      the draft row's entries in the order (value descending, index
+ *               ascending), read from logits row u of sequence b;
+ *   alternatives the ranked tokens other than chain_tok[b][u], best first;
+ *   b_s         Eq. (3) on margin m = margin[b*rows + u]:
+ *                 t = b_min + clip(1 - m / margin_scale, 0, 1) * (b_max - b_min)
+ *                 b_s = clip(round_half_even(t), b_min, b_max)
+ *               in float32, every operation rounded once; a NaN margin counts
+ *               as certain (b_s = b_min);
+ *   granted     min(b_s, remaining / branch_depth): whole branches only,
+ *               remaining starting at repair_budget, slots taken in order.
+ * Branch r of slot s is a chain of branch_depth nodes: its root carries
+ * alternative r and hangs off chain node u - 1 (-1, the context, when u = 0);
+ * node j > 0 carries suffix[b][u][r][j-1] (the token the drafter proposed
+ * after that substitution) or -1 when suffix is NULL, and hangs off node j - 1.
+ *
+ * Node numbering (the tree is in topological order): nodes 0 .. chain_len-1 are
+ * the chain (parent[i] = i - 1, token = chain_tok); then the branches, slot by
+ * slot and within a slot by alternative rank, each branch's nodes consecutive.
+ *
+ * Layout:
+ *   logits     [batch][rows][ld] dtype (the draft block's rows; the first
+ *              chain_len rows of each sequence are the chain positions)
+ *   margin     [batch][rows] float32, as cure_margins wrote it
+ *   ufp_pos    [batch][chain_len] int32, ufp_cnt [batch] int32, as cure_margins
+ *              wrote them (the slots used are the first min(ufp_cnt,
+ *              repair_budget / branch_depth), cut at the first position
+ *              outside [0, chain_len))
+ *   chain_tok  [batch][chain_len] int32, the draft block
+ *   suffix     [batch][chain_len][b_max][branch_depth-1] int32, or NULL
+ *   parent, token  [batch][n_max] int32 outputs; entries at or past
+ *              n_nodes[b] are not written
+ *   n_nodes    [batch] int32 output: chain_len + branch_depth * (branches)
+ *   branch_cnt [batch][chain_len] int32 output (may be NULL): branches granted
+ *              per slot, 0 for unused slots
+ * Requires 1 <= chain_len <= min(rows, 1024), branch_depth >= 1,
+ * repair_budget >= 0, 0 <= b_min <= b_max <= 7, b_max >= 1,
+ * vocab >= b_max + 1, vocab <= 524288, ld >= vocab, margin_scale > 0 and
+ * finite, n_max >= chain_len + repair_budget (so every tree fits).
+ * workspace: cure_repair_tree_workspace_size(...) bytes for the same arguments.
+ */
+size_t cure_repair_tree_workspace_size(int32_t batch, int32_t chain_len, int32_t vocab,
+                                       int32_t repair_budget, int32_t branch_depth);
+
+cure_status cure_repair_tree(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
+                             int32_t vocab, int64_t ld, const float* margin,
+                             const int32_t* ufp_pos, const int32_t* ufp_cnt,
+                             const int32_t* chain_tok, int32_t chain_len,
+                             int32_t repair_budget, int32_t branch_depth, float margin_scale,
+                             int32_t b_min, int32_t b_max, const int32_t* suffix,
+                             int32_t n_max, int32_t* parent, int32_t* token, int32_t* n_nodes,
+                             int32_t* branch_cnt, void* workspace, size_t workspace_bytes,
+                             void* stream);
 
 #ifdef __cplusplus
 }

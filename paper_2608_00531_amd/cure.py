@@ -46,6 +46,10 @@ _SIGNATURES = {
                                       _u32, _vp, _vp, _sz, _vp]),
     "cure_accept": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
                                    _vp, _vp, _vp, _vp, _vp, _vp]),
+    "cure_repair_tree_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "cure_repair_tree": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp,
+                                        _i32, _i32, _i32, _f32, _i32, _i32, _vp, _i32,
+                                        _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
 }
 
 
@@ -215,4 +219,50 @@ def cure_accept(parent, token, tgt, root_tgt, n_nodes, chain_len):
                            _ptr(out["acc_len"]), _ptr(out["path"]), _ptr(out["best"]),
                            _ptr(out["bonus"]), _ptr(out["resync"]), _stream(dev))
     _check(st, "cure_accept")
+    return out
+
+
+def cure_repair_tree(logits, margin, ufp_pos, ufp_cnt, chain_tok, repair_budget, branch_depth,
+                     margin_scale, b_min=1, b_max=5, suffix=None, n_max=None):
+    """Repair tree per sequence.
+
+    logits [batch, rows, vocab] (or [rows, vocab]) -- the draft block's rows;
+    margin [batch, rows] float32, ufp_pos [batch, chain_len], ufp_cnt [batch] as
+    cure_margins returned them; chain_tok int32 [batch, chain_len]; suffix int32
+    [batch, chain_len, b_max, branch_depth - 1] or None.
+    Returns a dict: parent, token [batch, n_max] (valid below n_nodes), n_nodes
+    [batch], branch_cnt [batch, chain_len].
+    """
+    _require_cuda(logits, margin, ufp_pos, ufp_cnt, chain_tok, suffix)
+    x = logits if logits.dim() == 3 else logits.unsqueeze(0)
+    if x.stride(2) != 1 or x.stride(0) != x.shape[1] * x.stride(1):
+        x = x.contiguous()
+    batch, rows, vocab = x.shape
+    chain_len = chain_tok.shape[-1]
+    if margin.dtype != torch.float32 or any(
+            t is not None and t.dtype != torch.int32 for t in (ufp_pos, ufp_cnt, chain_tok, suffix)):
+        raise CureError("margin must be float32; ufp_pos, ufp_cnt, chain_tok and suffix int32")
+    shapes = [(margin, (batch, rows)), (ufp_pos, (batch, chain_len)), (ufp_cnt, (batch,)),
+              (chain_tok, (batch, chain_len))]
+    if suffix is not None and branch_depth > 1:
+        shapes.append((suffix, (batch, chain_len, b_max, branch_depth - 1)))
+    for t, shape in shapes:
+        if tuple(t.shape) != shape:
+            raise CureError("expected shape %s, got %s" % (shape, tuple(t.shape)))
+    args = [t.contiguous() for t in (margin, ufp_pos, ufp_cnt, chain_tok)]
+    suffix = None if suffix is None or branch_depth == 1 else suffix.contiguous()
+    n_max = chain_len + repair_budget if n_max is None else n_max
+    dev = x.device
+    i = dict(dtype=torch.int32, device=dev)
+    out = {"parent": torch.empty(batch, n_max, **i), "token": torch.empty(batch, n_max, **i),
+           "n_nodes": torch.empty(batch, **i), "branch_cnt": torch.empty(batch, chain_len, **i)}
+    L = lib()
+    ws, wsb = _workspace("repair", dev, L.cure_repair_tree_workspace_size(
+        batch, chain_len, vocab, repair_budget, branch_depth))
+    st = L.cure_repair_tree(_ptr(x), _dtype_code(x), batch, rows, vocab, x.stride(1),
+                            *[_ptr(t) for t in args], chain_len, repair_budget, branch_depth,
+                            margin_scale, b_min, b_max, _ptr(suffix), n_max,
+                            _ptr(out["parent"]), _ptr(out["token"]), _ptr(out["n_nodes"]),
+                            _ptr(out["branch_cnt"]), _ptr(ws), wsb, _stream(dev))
+    _check(st, "cure_repair_tree")
     return out

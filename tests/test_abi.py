@@ -135,3 +135,51 @@ def test_binding_fails_loudly_without_gpu_tensors():
     import torch
     with pytest.raises(pc.CureError):
         pc.cure_margins(torch.zeros(2, 16))
+
+
+def _repair(L, **kw):
+    # 16 chain rows, vocab 32000, budget 16 in depth-4 branches: 4 UFP slots, so
+    # a missing workspace is reported before any launch.
+    args = dict(logits=1, dtype=1, batch=1, rows=16, vocab=32000, ld=32000, margin=1,
+                ufp_pos=1, ufp_cnt=1, chain_tok=1, chain_len=16, budget=16, depth=4,
+                scale=1.0, b_min=1, b_max=5, suffix=None, n_max=32, parent=1, token=1,
+                n_nodes=1, branch_cnt=None, workspace=None, ws_bytes=0, stream=None)
+    args.update(kw)
+    return L.cure_repair_tree(*args.values())
+
+
+def test_repair_argument_errors(L):
+    E, U = pc.CURE_ERR_INVALID_ARG, pc.CURE_ERR_UNSUPPORTED
+    assert _repair(L, dtype=3) == E
+    assert _repair(L, batch=-1) == E
+    assert _repair(L, batch=0) == pc.CURE_OK
+    assert _repair(L, chain_len=0) == E
+    assert _repair(L, rows=8) == E                         # rows < chain_len
+    assert _repair(L, depth=0) == E
+    assert _repair(L, budget=-1) == E
+    assert _repair(L, b_min=-1) == E
+    assert _repair(L, b_min=3, b_max=2) == E
+    assert _repair(L, b_min=0, b_max=0) == E
+    assert _repair(L, vocab=5, ld=5) == E                  # fewer than b_max + 1 entries
+    assert _repair(L, ld=100) == E
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert _repair(L, scale=bad) == E
+    assert _repair(L, n_max=31) == E                       # a full tree would not fit
+    for name in ("logits", "margin", "ufp_pos", "ufp_cnt", "chain_tok", "parent", "token",
+                 "n_nodes"):
+        assert _repair(L, **{name: None}) == E, name
+    assert _repair(L, b_max=8) == U
+    assert _repair(L, rows=1025, chain_len=1025, n_max=2000) == U
+    assert _repair(L, vocab=524289, ld=524289) == U
+    assert _repair(L) == pc.CURE_ERR_WORKSPACE
+
+
+def test_repair_workspace_size(L):
+    f = L.cure_repair_tree_workspace_size
+    assert f(1, 16, 32000, 3, 4) == 0                      # budget below one branch
+    assert f(0, 16, 32000, 16, 4) == 0
+    one = f(1, 16, 32000, 16, 4)
+    assert one > 0 and one % 256 == 0
+    assert f(4, 16, 32000, 16, 4) >= 4 * one - 512
+    assert f(1, 16, 128256, 16, 4) > one                   # more chunks per row
+    assert f(1, 16, 32000, 64, 4) > one                    # more UFP slots
