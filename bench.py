@@ -7,6 +7,10 @@ already resident in HBM:
   2. cure_tree_attn one tree-masked verification attention layer (Sec. 3.5),
   3. cure_accept    the acceptance walk, fed the margins' top-1 indices as the
                     target argmax (Eq. 1, Eq. 4).
+The repair-tree builder (cure_repair_tree: ranked alternatives at the UFPs,
+Eq. 3 branch budget, parent/token assembly) is timed beside the step, on the
+draft-chain rows and UFPs the step's margin pass produced; it is reported
+under `repair_tree` and is not part of `value`.
 
 Timing: each input copy's step is captured once as a HIP graph; W warm-up
 replays, then exactly K replays (K steps) bracketed by synchronize() on both
@@ -48,7 +52,10 @@ CSRC = os.path.join(ROOT, "paper_2608_00531_amd", "csrc")
 # Kernel sources behind each call: a stored traffic figure is used only while
 # these files are unchanged since the counters were taken.
 CALL_SOURCES = {"margins": ["margins.hip", "common.hpp"], "attn": ["tree_attn.hip", "common.hpp"],
-                "accept": ["accept.hip", "common.hpp"]}
+                "accept": ["accept.hip", "common.hpp"], "repair": ["repair.hip", "common.hpp"]}
+# Eq. 3 parameters of the repair-tree builder: the paper's b_min, b_max, and a
+# margin scale equal to the UFP threshold tau.
+B_MIN, B_MAX = 1, 5
 
 
 def parse():
@@ -84,6 +91,11 @@ class Step:
         self.status = torch.empty(B, **i32)
         self.acc = {k: torch.empty(B, **i32) for k in ("acc_len", "best", "bonus", "resync")}
         self.path = torch.empty(B, R, **i32)
+        K, budget, depth = w.chain_len, w.repair_budget, w.branch_depth
+        self.rep_nmax = K + budget
+        self.rep = {"parent": torch.empty(B, self.rep_nmax, **i32),
+                    "token": torch.empty(B, self.rep_nmax, **i32),
+                    "n_nodes": torch.empty(B, **i32), "branch_cnt": torch.empty(B, K, **i32)}
         self.host_ctx = np.ascontiguousarray(w.ctx_len, np.int32)
         self.host_nn = np.ascontiguousarray(w.n_nodes, np.int32)
         hc = self.host_ctx.ctypes.data_as(ctypes.c_void_p)
@@ -92,6 +104,8 @@ class Step:
         self.mws = torch.zeros(max(mws, 256), dtype=torch.uint8, device=dev)
         aws = L.cure_tree_attn_workspace_size(B, w.hq, w.hkv, w.d, R, hc, hn, 0)
         self.aws = torch.zeros(max(aws, 256), dtype=torch.uint8, device=dev)
+        rws = L.cure_repair_tree_workspace_size(B, K, V, budget, depth)
+        self.rws = torch.zeros(max(rws, 256), dtype=torch.uint8, device=dev)
         P = lambda t: ctypes.c_void_p(t.data_ptr())
         s = ctypes.c_void_p(stream)
         self.margins_args = (
@@ -110,6 +124,12 @@ class Step:
             P(copy["parent"]), P(copy["token"]), P(self.m["top1_idx"]), P(copy["root_tgt"]),
             P(copy["n_nodes"]), w.chain_len, B, R, P(self.acc["acc_len"]), P(self.path),
             P(self.acc["best"]), P(self.acc["bonus"]), P(self.acc["resync"]), s)
+        self.repair_args = (
+            P(copy["logits"]), pc.CURE_BF16 if w.dtype == "bf16" else pc.CURE_F32, B, R, V, V,
+            P(self.m["margin"]), P(self.ufp_pos), P(self.ufp_cnt), P(copy["chain_tok"]), K,
+            budget, depth, ctypes.c_float(w.tau), B_MIN, B_MAX, P(copy["suffix"]),
+            self.rep_nmax, P(self.rep["parent"]), P(self.rep["token"]),
+            P(self.rep["n_nodes"]), P(self.rep["branch_cnt"]), P(self.rws), self.rws.numel(), s)
 
     def margins(self):
         st = self.L.cure_margins(*self.margins_args)
@@ -126,6 +146,11 @@ class Step:
         if st:
             raise RuntimeError("cure_accept status %d" % st)
 
+    def repair(self):
+        st = self.L.cure_repair_tree(*self.repair_args)
+        if st:
+            raise RuntimeError("cure_repair_tree status %d" % st)
+
     def run(self):
         self.margins()
         self.attn()
@@ -139,10 +164,16 @@ def upload_copy(torch, w):
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
         return torch.from_numpy(a).cuda()
     bf = w.dtype == "bf16"
+    # Suffix tokens the drafter would propose after each substitution: seeded
+    # uniform tokens [batch][chain_len][b_max][branch_depth - 1].
+    rng = np.random.default_rng(np.random.SeedSequence([w.seed, 99]))
+    suffix = rng.integers(0, w.vocab, size=(w.batch, w.chain_len, B_MAX,
+                                           max(w.branch_depth - 1, 1))).astype(np.int32)
     return {
         "logits": dev(w.logits, bf), "q": dev(w.q, bf), "k": dev(w.k, bf), "v": dev(w.v, bf),
         "kv_off": dev(w.kv_off), "ctx_len": dev(w.ctx_len), "n_nodes": dev(w.n_nodes),
         "parent": dev(w.parent), "token": dev(w.token), "root_tgt": dev(w.root_tgt),
+        "chain_tok": dev(w.token[:, :w.chain_len]), "suffix": dev(suffix),
     }
 
 
@@ -191,11 +222,11 @@ def timed_steps(torch, graphs, k, warmup):
 def per_call_times(torch, steps, k):
     """Average GPU duration of each call, from events around every eager launch.
     A spin kernel queued first keeps the host's launch cost off the GPU timeline."""
-    names = ("margins", "attn", "accept")
+    names = ("margins", "attn", "accept", "repair")
     n = len(steps)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(k)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(k)]
     torch.cuda.synchronize()
-    spin(torch, 20000)
+    spin(torch, 25000)
     for i in range(k):
         s = steps[i % n]
         ev[i][0].record()
@@ -205,6 +236,8 @@ def per_call_times(torch, steps, k):
         ev[i][2].record()
         s.accept()
         ev[i][3].record()
+        s.repair()
+        ev[i][4].record()
     torch.cuda.synchronize()
     out = {}
     for j, name in enumerate(names):
@@ -229,6 +262,26 @@ def stored_traffic(call, workload):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return int(entry["bytes_per_call"]) if h.hexdigest() == entry["sources_sha256"] else None
+
+
+def repair_bytes(w, step):
+    """Algorithmic bytes of one cure_repair_tree call, from what it produced: the
+    logits rows of the UFPs that received branches (the rows that must be
+    ranked), the UFP list, count and margins, the draft block, the suffix tokens
+    of the granted branches, and the parent/token arrays, node count and
+    per-UFP branch counts written."""
+    bc = step.rep["branch_cnt"].cpu().numpy()
+    nn = step.rep["n_nodes"].cpu().numpy()
+    eb = w.elem_bytes()
+    ranked = int((bc > 0).sum())
+    branches = int(bc.sum())
+    K = w.chain_len
+    total = (ranked * w.vocab * eb + w.batch * (3 * K * 4 + 4)
+             + branches * (w.branch_depth - 1) * 4
+             + int(nn.sum()) * 8 + w.batch * (4 + K * 4))
+    info = {"rows_ranked": ranked, "branches": branches, "nodes": int(nn.sum()),
+            "bytes": total}
+    return total, info
 
 
 def cpu_baseline(w, algo_bytes, budget_s):
@@ -285,6 +338,7 @@ def main():
         steps = [Step(pc, torch, w, c, stream.cuda_stream) for c in copies]
         for st in steps:                       # eager reference results, one per copy
             st.run()
+            st.repair()
         torch.cuda.synchronize()
         ref = [(st.m["top1_idx"].clone(), st.acc["acc_len"].clone(), st.o.clone())
                for st in steps]
@@ -298,14 +352,17 @@ def main():
     status = steps[0].status.cpu().tolist()
     assert status == [0] * w.batch, status
     acc_len = steps[0].acc["acc_len"].float().cpu()
+    rep_bytes, rep_info = repair_bytes(w, steps[0])
 
-    call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"]}
+    call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"],
+                  "repair": rep_bytes}
     kernels = {}
     for name, us in calls.items():
         gbs = call_bytes[name] / (us * 1e-6) / 1e9
         kernels[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
                          "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
-    dom = max(calls, key=calls.get)
+    step_calls = {k: v for k, v in calls.items() if k != "repair"}
+    dom = max(step_calls, key=step_calls.get)
     dom_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
     names = {"margins": "cure_margins (margins_kernel)",
              "attn": "cure_tree_attn (tree_attn_m16 or tree_attn_mfma, + attn_merge)",
@@ -338,6 +395,13 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
                      "traffic": stored_traffic(dom, w.name)},
+        "repair_tree": dict(rep_info, us=round(calls["repair"], 2),
+                            roofline={"bound": "hbm", "kernel": "cure_repair_tree (topk_chunk "
+                                      "+ repair_assemble)",
+                                      "achieved": kernels["repair"]["GB/s"],
+                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                      "frac": kernels["repair"]["frac_hbm"],
+                                      "traffic": stored_traffic("repair", w.name)}),
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)

@@ -9,17 +9,23 @@
 //   free: within a wave, the minimum over eight 8-lane groups of the group
 //   maximum is reached by eight distinct entries, so no entry below it can be
 //   among the chunk's best eight. The workgroup takes the largest such bound
-//   over its waves, appends the few entries at or above it to LDS, and one
-//   wave ranks them exactly. Only when more than kCandCap entries pass (large
-//   runs of equal values) does the workgroup fall back to eight rounds of
-//   workgroup-wide selection over the registers. Output: the chunk's best
-//   eight (value descending, index ascending) in the workspace.
+//   over its waves; each wave appends its entries at or above it to its LDS
+//   list (ballot and lane count, no atomics), and every candidate finds its
+//   rank by counting the candidates that outrank it. Only when a wave has more
+//   than kWaveCap candidates (large runs of equal values) does the workgroup
+//   fall back to eight rounds of workgroup-wide selection over the registers.
+//   Output: the chunk's best eight (value descending, index ascending) in the
+//   workspace.
 //
-// repair_assemble -- one workgroup per sequence. Each wave merges the chunk
-//   results of a UFP row into the row's best eight, drops the draft's own
-//   token to get the ranked alternatives, and evaluates Eq. (3) on the row's
-//   margin. One lane then walks the UFPs in order and hands out whole branches
-//   while they fit the budget; finally all lanes write the parent/token arrays.
+// repair_assemble -- one workgroup per sequence. Eq. (3) on each UFP's margin,
+//   then one wave walks the UFPs in order and hands out whole branches while
+//   they fit the budget. Each wave takes a UFP row that received branches,
+//   writes its branches' suffix nodes, merges the row's chunk results into
+//   its best eight and writes the branch roots: the ranked tokens without the
+//   draft's own.
+//
+// The chunk kernel makes the same budget walk up front (from the margins
+// alone) and skips the rows of UFPs that the budget leaves without branches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -38,13 +44,33 @@ constexpr int kVec = 8;                  // entries per 16-byte bf16 vector
 constexpr int kLaneVecs = 4;             // vectors per lane per chunk
 constexpr int kChunk = kThreads * kVec * kLaneVecs;   // 8192 entries
 constexpr int kMaxSplits = 64;
-constexpr int kCandCap = 256;            // LDS candidates per chunk
+constexpr int kWaveCap = 64;             // LDS candidates per wave
 constexpr int kMaxChain = 1024;
+
+// A ranked entry: value and vocabulary index. 8-byte aligned so that one LDS
+// access moves a whole record.
+struct __attribute__((aligned(8))) Cand {
+  float v;
+  int i;
+};
+
+// (va, ia) ranks before (vb, ib): larger value, or equal value and lower index.
+// Written with bitwise operators so that no operand is evaluated lazily (a
+// lazy operand becomes a branch around its load).
+CURE_DEV bool outranks(float va, int ia, float vb, int ib) {
+  return (va > vb) | ((va == vb) & (ia < ib));
+}
+
+// Number of set bits of m in lanes below this one.
+CURE_DEV int lanes_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
 
 struct Args {
   const void* logits;
   int64_t ld;
-  int32_t rows, vocab, splits, max_slots, chain_len;
+  int32_t batch, rows, vocab, splits, max_slots, chain_len;
   const float* margin;
   const int32_t* ufp_pos;
   const int32_t* ufp_cnt;
@@ -115,52 +141,151 @@ CURE_DEV void wave_best(float& bv, int& bi) {
   best_stage<32>(bv, bi);
 }
 
-// Exact best eight over the wave's candidates: lane l holds kPer of them
-// (empty = (-inf, INT32_MAX), which every real entry beats; real indices are
-// distinct). Eight rounds of a wave-wide best, each removing its winner.
-// Lane r < 8 returns the r-th best; every lane must take part.
-template <int kPer>
-CURE_DEV void wave_top8(float (&v)[kPer], int (&ix)[kPer], float& ov, int& oi) {
+// Eq. (3): u = clip(1 - m / s, 0, 1), b = clip(round(b_min + u (b_max - b_min)),
+// b_min, b_max), each operation rounded once to float32 and round() to the
+// nearest even integer. A NaN margin gives u = 0 (fmaxf drops the NaN).
+CURE_DEV int branch_budget(float m, float s, int lo, int hi) {
+#pragma clang fp contract(off)
+  float u = 1.0f - m / s;
+  u = fminf(fmaxf(u, 0.0f), 1.0f);
+  const float t = (float)lo + u * (float)(hi - lo);
+  const int bb = (int)rintf(t);
+  return min(max(bb, lo), hi);
+}
+
+// Whether the budget walk (the one repair_assemble makes) grants UFP slot
+// `slot` of sequence b any branch; false also when this or an earlier slot's
+// position lies outside the block (the slot list ends there). Every lane of
+// the wave must take part. When even the largest possible grants to the
+// earlier slots (b_max branches each) leave room for a branch, and b_min >= 1,
+// the answer needs no margins: that saves the dependent read of the margins
+// for the first slots. Otherwise each lane evaluates Eq. (3) for one slot and
+// the walk reads the results lane by lane.
+CURE_DEV bool slot_has_branches(const Args& a, int b, int slot) {
   const int lane = lane_id();
-  ov = -INFINITY;
-  oi = INT32_MAX;
-#pragma unroll
-  for (int r = 0; r < kTopK; ++r) {
-    float bv = v[0];
-    int bi = ix[0];
-#pragma unroll
-    for (int k = 1; k < kPer; ++k) {
-      const bool c = beats(v[k], ix[k], bv, bi);
-      bv = c ? v[k] : bv;
-      bi = c ? ix[k] : bi;
+  const int K = a.chain_len;
+  const bool sure = a.b_min >= 1 && ((int64_t)slot * a.b_max + 1) * a.depth <= a.budget;
+  int remaining = a.budget;
+  for (int g0 = 0; g0 <= slot; g0 += kWave) {
+    const int s = g0 + lane;
+    const int us = s <= slot ? a.ufp_pos[(int64_t)b * K + s] : 0;
+    if (__ballot(us < 0 || us >= K)) return false;
+    if (sure) continue;
+    const int bs = s <= slot ? branch_budget(a.margin[(int64_t)b * a.rows + us], a.scale,
+                                             a.b_min, a.b_max)
+                             : 0;
+    const int last = min(slot - g0, kWave - 1);
+    for (int i = 0; i <= last; ++i) {
+      const int nb = min(__builtin_amdgcn_readlane(bs, i), remaining / a.depth);
+      if (g0 + i == slot) return nb > 0;
+      remaining -= nb * a.depth;
     }
-    wave_best(bv, bi);
-    ov = lane == r ? bv : ov;
-    oi = lane == r ? bi : oi;
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const bool hit = ix[k] == bi;
-      v[k] = hit ? -INFINITY : v[k];
-      ix[k] = hit ? INT32_MAX : ix[k];
-    }
+  }
+  return true;
+}
+
+// Rank of the record (mv, mi) among n records in LDS: how many outrank it.
+// The records' indices are distinct, so ranks are distinct. All lanes read
+// the same record in each step (an LDS broadcast).
+CURE_DEV int rank_among(const Cand* c, int n, float mv, int mi) {
+  int rank = 0;
+#pragma unroll 8
+  for (int k = 0; k < n; ++k) {
+    const Cand o = c[k];
+    rank += outranks(o.v, o.i, mv, mi) ? 1 : 0;
+  }
+  return rank;
+}
+
+// Lane exchanges for merging sorted 8-entry lists held one entry per lane, a
+// list in each aligned group of 8 lanes (entry p in lane 8g + p).
+//   xor1, xor2     DPP quad permutes
+//   xor4           swizzle, lane ^ 4 within 32
+//   mirror8        lane 8g + p <-> 8g + 7 - p (DPP half-row mirror)
+//   mirror16/32/64 lane i <-> 15 - i / 31 - i / 63 - i within 16 / 32 / 64
+//                  (DPP row mirror; swizzle lane ^ 31; that plus permlane32)
+enum Xchg { kXor1, kXor2, kXor4, kMirror8, kMirror16, kMirror32, kMirror64 };
+
+template <Xchg kX>
+CURE_DEV int xchg(int v) {
+  if (kX == kXor1) return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  if (kX == kXor2) return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  if (kX == kXor4) return __builtin_amdgcn_ds_swizzle(v, 0x101F);
+  if (kX == kMirror8) return __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+  if (kX == kMirror16) return __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  const int m32 = __builtin_amdgcn_ds_swizzle(v, 0x7C1F);
+  if (kX == kMirror32) return m32;
+  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)m32, (unsigned)m32, false, false);
+  return (int)(lane_id() < 32 ? r[1] : r[0]);
+}
+
+// One compare-exchange of a bitonic network: the lane whose position has bit
+// kBit clear keeps the better record of itself and its partner, the other
+// lane the worse.
+template <Xchg kX, int kBit>
+CURE_DEV void cmp_xchg(float& v, int& i) {
+  const float ov = __int_as_float(xchg<kX>(__float_as_int(v)));
+  const int oi = xchg<kX>(i);
+  const bool keep_better = (lane_id() & kBit) == 0;
+  const bool take = keep_better ? outranks(ov, oi, v, i) : outranks(v, i, ov, oi);
+  v = take ? ov : v;
+  i = take ? oi : i;
+}
+
+// Sorts a bitonic sequence of 8 records held by an 8-lane group, best first.
+CURE_DEV void clean8(float& v, int& i) {
+  cmp_xchg<kXor4, 4>(v, i);
+  cmp_xchg<kXor2, 2>(v, i);
+  cmp_xchg<kXor1, 1>(v, i);
+}
+
+// The best 8 of two sorted lists, sorted: (v, i) is entry p of one list and
+// (ov, oi) entry 7 - p of the other (a mirrored partner), so the better of
+// the two forms a bitonic sequence over the group.
+CURE_DEV void merge8(float& v, int& i, float ov, int oi) {
+  const bool take = outranks(ov, oi, v, i);
+  v = take ? ov : v;
+  i = take ? oi : i;
+  clean8(v, i);
+}
+
+// Merges the list of this lane's group with the list of the group mirrored
+// across kX; afterwards both groups hold the merged list.
+template <Xchg kX>
+CURE_DEV void merge_groups(float& v, int& i) {
+  merge8(v, i, __int_as_float(xchg<kX>(__float_as_int(v))), xchg<kX>(i));
+}
+
+// Appends this lane's record to the wave's LDS list when keep is set, in lane
+// order, without atomics: the slot is the wave's running count plus the
+// number of keeping lanes below. Records past kWaveCap are dropped but still
+// counted. The branch on the ballot is uniform across the wave.
+CURE_DEV void wave_append(Cand* list, int& count, bool keep, float v, int i) {
+  const uint64_t m = __ballot(keep);
+  if (m) {
+    const int slot = count + lanes_below(m);
+    if (keep && slot < kWaveCap) list[slot] = Cand{v, i};
+    count += __popcll(m);
   }
 }
 
 template <typename T, bool kVecPath>
 __global__ __launch_bounds__(kThreads) void topk_chunk(Args a) {
-  __shared__ float s_cv[kCandCap];
-  __shared__ int s_ci[kCandCap];
+  __shared__ Cand s_cand[kWaves][kWaveCap];
+  __shared__ Cand s_top[kWaves][kTopK];
   __shared__ float s_bound[kWaves];
-  __shared__ float s_rv[kWaves];
-  __shared__ int s_ri[kWaves];
-  __shared__ int s_cnt;
 
+  // Slot-major order: the budget grants branches to a prefix of each
+  // sequence's slots, so the workgroups that find work are dispatched first.
   const int split = blockIdx.x % a.splits;
-  const int slot = (blockIdx.x / a.splits) % a.max_slots;
-  const int b = blockIdx.x / (a.splits * a.max_slots);
-  if (slot >= min(a.ufp_cnt[b], a.max_slots)) return;
+  const int b = (blockIdx.x / a.splits) % a.batch;
+  const int slot = blockIdx.x / (a.splits * a.batch);
+  // Unused slots and slots that the budget leaves without branches need no
+  // ranking. (Positions below max_slots are always readable.)
+  const int listed = a.ufp_cnt[b];
+  const bool granted = slot_has_branches(a, b, slot);
+  if (slot >= min(listed, a.max_slots) || !granted) return;
   const int u = a.ufp_pos[(int64_t)b * a.chain_len + slot];
-  if (u < 0 || u >= a.chain_len) return;
 
   const T* x = reinterpret_cast<const T*>(a.logits) + ((int64_t)b * a.rows + u) * a.ld;
   const int begin = split * kChunk;
@@ -222,196 +347,223 @@ __global__ __launch_bounds__(kThreads) void topk_chunk(Args a) {
   g = fminf(g, partner<16>(g));
   g = fminf(g, partner<32>(g));
   if (lane == 0) s_bound[wave] = g;
-  if (tid == 0) s_cnt = 0;
   __syncthreads();
   const float bound = fmaxf(fmaxf(s_bound[0], s_bound[1]), fmaxf(s_bound[2], s_bound[3]));
 
-  // Candidates: the entries at or above the bound.
+  // Candidates: the entries at or above the bound, appended per wave.
+  int wcnt = 0;
 #pragma unroll
   for (int w = 0; w < kLaneVecs; ++w) {
-    if (vmax[w] >= bound) {
-      const int e0 = (w * kThreads + tid) * kVec;
+    const int e0 = (w * kThreads + tid) * kVec;
 #pragma unroll
-      for (int j = 0; j < kVec; ++j) {
-        if (e0 + j < n && f[w][j] >= bound) {
-          const int p = atomicAdd(&s_cnt, 1);
-          if (p < kCandCap) {
-            s_cv[p] = f[w][j];
-            s_ci[p] = begin + e0 + j;
-          }
+    for (int j = 0; j < kVec; ++j)
+      wave_append(s_cand[wave], wcnt, (e0 + j < n) & (f[w][j] >= bound), f[w][j], begin + e0 + j);
+  }
+  const int64_t out = (((int64_t)b * a.max_slots + slot) * a.splits + split) * kTopK;
+
+  // Each wave's best eight, sorted, into s_top: every candidate finds its rank
+  // among the wave's candidates by counting those that outrank it; places
+  // beyond the count stay empty. A wave with more candidates than its list
+  // holds (long runs of equal values) ranks its registers in eight rounds of
+  // a wave-wide best instead.
+  if (lane < kTopK) s_top[wave][lane] = Cand{-INFINITY, INT32_MAX};
+  __builtin_amdgcn_wave_barrier();
+  if (wcnt <= kWaveCap) {
+    if (lane < wcnt) {
+      const Cand m = s_cand[wave][lane];
+      const int rank = rank_among(s_cand[wave], wcnt, m.v, m.i);
+      if (rank < kTopK) s_top[wave][rank] = m;
+    }
+  } else {
+    uint32_t taken = 0;
+    for (int r = 0; r < kTopK; ++r) {
+      float bv = -INFINITY;
+      int bi = INT32_MAX;
+#pragma unroll
+      for (int w = 0; w < kLaneVecs; ++w) {
+        const int e0 = (w * kThreads + tid) * kVec;
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+          const bool ok = (e0 + j < n) & !((taken >> (w * kVec + j)) & 1u);
+          const bool c = ok & outranks(f[w][j], begin + e0 + j, bv, bi);
+          bv = c ? f[w][j] : bv;
+          bi = c ? begin + e0 + j : bi;
         }
       }
+      wave_best(bv, bi);
+      if (lane == 0) s_top[wave][r] = Cand{bv, bi};
+      const int rel = bi - begin;                 // chunk entry of the winner
+      if (bi != INT32_MAX && (rel / kVec) % kThreads == tid)
+        taken |= 1u << ((rel / kVec / kThreads) * kVec + rel % kVec);
     }
   }
   __syncthreads();
-  const int cnt = s_cnt;
-  const int64_t out = (((int64_t)b * a.max_slots + slot) * a.splits + split) * kTopK;
 
-  if (cnt <= kCandCap) {
-    if (wave == 0) {
-      float cv[kCandCap / kWave];
-      int ci[kCandCap / kWave];
-#pragma unroll
-      for (int q = 0; q < kCandCap / kWave; ++q) {
-        const int c = lane + q * kWave;
-        cv[q] = c < cnt ? s_cv[c] : -INFINITY;
-        ci[q] = c < cnt ? s_ci[c] : INT32_MAX;
-      }
-      float ov;
-      int oi;
-      wave_top8(cv, ci, ov, oi);
-      if (lane < kTopK) {
-        a.part_val[out + lane] = ov;
-        a.part_idx[out + lane] = oi;
-      }
+  // The four sorted lists, one per 8-lane group of wave 0, merged pairwise.
+  if (wave == 0) {
+    const Cand m = lane < kWaves * kTopK ? s_top[lane / kTopK][lane % kTopK]
+                                         : Cand{-INFINITY, INT32_MAX};
+    float v = m.v;
+    int i = m.i;
+    merge_groups<kMirror16>(v, i);
+    merge_groups<kMirror32>(v, i);
+    if (lane < kTopK) {
+      a.part_val[out + lane] = v;
+      a.part_idx[out + lane] = i;
     }
-    return;
-  }
-
-  // Too many ties at the bound: eight rounds of a workgroup-wide best over the
-  // registers, each round removing its winner (taken bits are per entry).
-  uint32_t taken = 0;
-  float rv = -INFINITY;
-  int ri = INT32_MAX;
-  for (int r = 0; r < kTopK; ++r) {
-    float bv = -INFINITY;
-    int bi = INT32_MAX;
-#pragma unroll
-    for (int w = 0; w < kLaneVecs; ++w) {
-      const int e0 = (w * kThreads + tid) * kVec;
-#pragma unroll
-      for (int j = 0; j < kVec; ++j) {
-        const bool ok = e0 + j < n && !((taken >> (w * kVec + j)) & 1u);
-        const bool c = ok && beats(f[w][j], begin + e0 + j, bv, bi);
-        bv = c ? f[w][j] : bv;
-        bi = c ? begin + e0 + j : bi;
-      }
-    }
-    wave_best(bv, bi);
-    if (lane == 0) { s_rv[wave] = bv; s_ri[wave] = bi; }
-    __syncthreads();
-    float gv = s_rv[0];
-    int gi = s_ri[0];
-#pragma unroll
-    for (int k = 1; k < kWaves; ++k) {
-      const bool c = beats(s_rv[k], s_ri[k], gv, gi);
-      gv = c ? s_rv[k] : gv;
-      gi = c ? s_ri[k] : gi;
-    }
-    __syncthreads();
-    const int rel = gi - begin;                 // chunk entry of the winner
-    const int owner_w = rel / kVec / kThreads, owner_t = rel / kVec % kThreads;
-    if (gi != INT32_MAX && owner_t == tid) taken |= 1u << (owner_w * kVec + rel % kVec);
-    rv = tid == r ? gv : rv;
-    ri = tid == r ? gi : ri;
-  }
-  if (tid < kTopK) {
-    a.part_val[out + tid] = rv;
-    a.part_idx[out + tid] = ri;
   }
 }
 
-// Eq. (3): u = clip(1 - m / s, 0, 1), b = clip(round(b_min + u (b_max - b_min)),
-// b_min, b_max), each operation rounded once to float32 and round() to the
-// nearest even integer. A NaN margin gives u = 0 (fmaxf drops the NaN).
-CURE_DEV int branch_budget(float m, float s, int lo, int hi) {
-#pragma clang fp contract(off)
-  float u = 1.0f - m / s;
-  u = fminf(fmaxf(u, 0.0f), 1.0f);
-  const float t = (float)lo + u * (float)(hi - lo);
-  const int bb = (int)rintf(t);
-  return min(max(bb, lo), hi);
+// Loads the chunk results of UFP slot s: lane l holds records l + 64 q. The
+// loads are unconditional (indices past the end are clamped and their values
+// replaced), so no branch forces a wait for them.
+CURE_DEV void load_partials(const Args& a, int b, int s, float (&cv)[kMaxSplits * kTopK / kWave],
+                            int (&ci)[kMaxSplits * kTopK / kWave]) {
+  const int lane = lane_id();
+  const int64_t base = (((int64_t)b * a.max_slots + s) * a.splits) * kTopK;
+  const int ncand = a.splits * kTopK;
+#pragma unroll
+  for (int q = 0; q < kMaxSplits * kTopK / kWave; ++q) {
+    const int c = lane + q * kWave;
+    const int cc = min(c, ncand - 1);
+    const float v = a.part_val[base + cc];
+    const int i = a.part_idx[base + cc];
+    cv[q] = c < ncand ? v : -INFINITY;
+    ci[q] = c < ncand ? i : INT32_MAX;
+  }
+}
+
+// The suffix token of branch node t (t = r * depth + j, j > 0) of the branch
+// at block position u, or -1 without suffix tokens.
+CURE_DEV int suffix_token(const Args& a, int b, int u, int t) {
+  const int r = t / a.depth, j = t - r * a.depth;
+  if (!a.suffix || j == 0) return -1;
+  return a.suffix[(((int64_t)b * a.chain_len + u) * a.b_max + r) * (a.depth - 1) + (j - 1)];
 }
 
 __global__ __launch_bounds__(kThreads) void repair_assemble(Args a) {
   extern __shared__ int s_dyn[];
-  int* s_alt = s_dyn;                               // [max_slots][kTopK]
-  int* s_nb = s_alt + a.max_slots * kTopK;          // [max_slots] Eq. (3), then granted
+  int* s_nb = s_dyn;                                // [max_slots] Eq. (3), then granted
   int* s_first = s_nb + a.max_slots;                // [max_slots] first branch number
+  int* s_u = s_first + a.max_slots;                 // [max_slots] block position
+  int* s_own = s_u + a.max_slots;                   // [max_slots] the draft's token there
   __shared__ int s_slots, s_total;
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int K = a.chain_len;
-  const int32_t* pos = a.ufp_pos + (int64_t)b * K;
+  const int K = a.chain_len, d = a.depth;
+  int32_t* par = a.parent + (int64_t)b * a.n_max;
+  int32_t* tok = a.token + (int64_t)b * a.n_max;
+  constexpr int kPer = kMaxSplits * kTopK / kWave;
 
-  // UFP slots in use: the first min(ufp_cnt, max_slots), cut at the first
-  // position outside the block.
-  if (tid == 0) s_slots = max(0, min(a.ufp_cnt[b], a.max_slots));
+  // On this GPU one counter tracks loads and stores together, so a wait for a
+  // load also waits for every store issued before it: all loads come first,
+  // grouped into as few round trips as the dependences allow, and every store
+  // is issued after the last wait.
+  //
+  // First round trip: the UFP count and positions, the draft block, and each
+  // wave's first slot's chunk results (read before it is known whether that
+  // slot received branches; unused if not). The slots in use are the first
+  // min(ufp_cnt, max_slots), cut at the first position outside the block.
+  const int listed = a.ufp_cnt[b];
+  const int u_first = a.ufp_pos[(int64_t)b * K + min(tid, max(a.max_slots, 1) - 1)];
+  const int chain_first = a.chain_tok[(int64_t)b * K + min(tid, K - 1)];
+  float cv[kPer];
+  int ci[kPer];
+  if (a.max_slots > 0) load_partials(a, b, min(wave, a.max_slots - 1), cv, ci);
+  if (tid == 0) s_slots = max(0, min(listed, a.max_slots));
   __syncthreads();
-  const int listed = s_slots;
-  __syncthreads();
-  for (int s = tid; s < listed; s += kThreads) {
-    const int u = pos[s];
-    if (u < 0 || u >= K) atomicMin(&s_slots, s);
+  // Second: each slot's margin for Eq. (3) and the draft's token at its position.
+  for (int s = tid; s < a.max_slots; s += kThreads) {
+    const int u = s == tid ? u_first : a.ufp_pos[(int64_t)b * K + s];
+    const bool ok = u >= 0 && u < K;
+    if (!ok) atomicMin(&s_slots, s);
+    s_u[s] = u;
+    s_own[s] = ok ? a.chain_tok[(int64_t)b * K + u] : -1;
+    s_nb[s] = ok ? branch_budget(a.margin[(int64_t)b * a.rows + u], a.scale, a.b_min, a.b_max) : 0;
   }
   __syncthreads();
   const int slots = s_slots;
 
-  // Per slot: the row's best eight from its chunk results, the ranked
-  // alternatives (the draft's own token removed) and Eq. (3).
-  constexpr int kPer = kMaxSplits * kTopK / kWave;
-  for (int s = wave; s < slots; s += kWaves) {
-    const int u = pos[s];
-    const int64_t base = (((int64_t)b * a.max_slots + s) * a.splits) * kTopK;
-    const int ncand = a.splits * kTopK;
-    float cv[kPer];
-    int ci[kPer];
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      const int c = lane + q * kWave;
-      cv[q] = c < ncand ? a.part_val[base + c] : -INFINITY;
-      ci[q] = c < ncand ? a.part_idx[base + c] : INT32_MAX;
+  // The budget walk on wave 0: whole branches of depth nodes, UFP by UFP,
+  // while they fit. Lane l holds slot g0 + l; the walk itself runs on scalars.
+  if (wave == 0) {
+    int remaining = a.budget, granted = 0;
+    for (int g0 = 0; g0 < slots; g0 += kWave) {
+      const int s = g0 + lane;
+      const int want = s < slots ? s_nb[s] : 0;
+      int my_nb = 0, my_first = 0;
+      const int n = min(slots - g0, kWave);
+      for (int i = 0; i < n; ++i) {
+        const int nb = min(__builtin_amdgcn_readlane(want, i), remaining / d);
+        my_nb = lane == i ? nb : my_nb;
+        my_first = lane == i ? granted : my_first;
+        granted += nb;
+        remaining -= nb * d;
+      }
+      if (s < slots) {
+        s_nb[s] = my_nb;
+        s_first[s] = my_first;
+      }
     }
-    float tv;
-    int ti;
-    wave_top8(cv, ci, tv, ti);
-    const int own = a.chain_tok[(int64_t)b * K + u];
+    if (lane == 0) s_total = granted;
+  }
+  __syncthreads();
+
+  // Per slot with branches, one wave: the row's best eight from its chunk
+  // results, the branch roots (alternative r, the r-th ranked token other than
+  // the draft's own, hangs off chain node u - 1), and the nodes past the roots
+  // (suffix tokens, or -1, each hanging off the node before it).
+  // The largest 8th entry over the chunk lists bounds the row's 8th best from
+  // below, so only the entries at or above it are ranked (by counting, as in
+  // the chunk kernel); if ties leave more than a wave's worth of them, eight
+  // rounds of a wave-wide best rank all entries instead.
+  for (int s = wave; s < slots; s += kWaves) {
+    const int nb = s_nb[s];
+    if (nb == 0) continue;
+    const int u = s_u[s];
+    const int first = K + s_first[s] * d;
+    const int nodes = nb * d;
+    // The first suffix token of this lane (issued now, stored after the merge).
+    const int sfx0 = lane < nodes ? suffix_token(a, b, u, lane) : -1;
+    if (s != wave) load_partials(a, b, s, cv, ci);
+    // Lane l holds entry l % 8 of chunk list l / 8 + 8 q in (cv[q], ci[q]);
+    // lists past the chunk count are empty. Fold the register lists
+    // pairwise, then the eight lists of the wave across lanes.
+    const int nq = (a.splits + kWave / kTopK - 1) / (kWave / kTopK);
+#pragma unroll
+    for (int step = 1; step < kPer; step *= 2)
+#pragma unroll
+      for (int q = 0; q + step < kPer; q += 2 * step)
+        if (q + step < nq)
+          merge8(cv[q], ci[q], __int_as_float(xchg<kMirror8>(__float_as_int(cv[q + step]))),
+                 xchg<kMirror8>(ci[q + step]));
+    float tv = cv[0];
+    int ti = ci[0];
+    merge_groups<kMirror16>(tv, ti);
+    merge_groups<kMirror32>(tv, ti);
+    merge_groups<kMirror64>(tv, ti);
+    const int own = s_own[s];
     const bool is_own = lane < kTopK && ti == own;
     const uint64_t own_mask = __ballot(is_own);
     const int own_rank = own_mask ? __builtin_ctzll(own_mask) : kTopK;
     const int alt_rank = lane - (own_rank < lane ? 1 : 0);
-    if (lane < kTopK && !is_own && alt_rank < a.b_max) s_alt[s * kTopK + alt_rank] = ti;
-    if (lane == 0)
-      s_nb[s] = branch_budget(a.margin[(int64_t)b * a.rows + u], a.scale, a.b_min, a.b_max);
-  }
-  __syncthreads();
-
-  // Whole branches of depth nodes, UFP by UFP, while they fit the budget.
-  if (tid == 0) {
-    int remaining = a.budget, granted = 0;
-    for (int s = 0; s < slots; ++s) {
-      const int nb = min(s_nb[s], remaining / a.depth);
-      s_nb[s] = nb;
-      s_first[s] = granted;
-      granted += nb;
-      remaining -= nb * a.depth;
+    if (lane < kTopK && !is_own && alt_rank < nb) {
+      par[first + alt_rank * d] = u - 1;
+      tok[first + alt_rank * d] = ti;
     }
-    s_total = granted;
+    for (int t = lane; t < nodes; t += kWave) {
+      if (t % d == 0) continue;
+      par[first + t] = first + t - 1;
+      tok[first + t] = t == lane ? sfx0 : suffix_token(a, b, u, t);
+    }
   }
-  __syncthreads();
 
-  int32_t* par = a.parent + (int64_t)b * a.n_max;
-  int32_t* tok = a.token + (int64_t)b * a.n_max;
+  // The chain, the per-slot branch counts and the node count.
   for (int i = tid; i < K; i += kThreads) {
     par[i] = i - 1;
-    tok[i] = a.chain_tok[(int64_t)b * K + i];
+    tok[i] = i == tid ? chain_first : a.chain_tok[(int64_t)b * K + i];
     if (a.branch_cnt) a.branch_cnt[(int64_t)b * K + i] = i < slots ? s_nb[i] : 0;
-  }
-  const int d = a.depth;
-  for (int s = 0; s < slots; ++s) {
-    const int u = pos[s];
-    const int first = K + s_first[s] * d;
-    for (int t = tid; t < s_nb[s] * d; t += kThreads) {
-      const int r = t / d, j = t - r * d;
-      const int node = first + t;
-      par[node] = j == 0 ? u - 1 : node - 1;
-      int tk;
-      if (j == 0) tk = s_alt[s * kTopK + r];
-      else if (a.suffix) tk = a.suffix[(((int64_t)b * K + u) * a.b_max + r) * (d - 1) + (j - 1)];
-      else tk = -1;
-      tok[node] = tk;
-    }
   }
   if (tid == 0) a.n_nodes[b] = K + s_total * d;
 }
@@ -471,6 +623,7 @@ extern "C" cure_status cure_repair_tree(
   Args a;
   a.logits = logits;
   a.ld = ld;
+  a.batch = batch;
   a.rows = rows;
   a.vocab = vocab;
   a.splits = splits;
@@ -510,7 +663,7 @@ extern "C" cure_status cure_repair_tree(
     }
     if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
   }
-  const size_t lds = (size_t)std::max(slots, 1) * (kTopK + 2) * sizeof(int);
+  const size_t lds = (size_t)std::max(slots, 1) * 4 * sizeof(int);
   hipLaunchKernelGGL(repair_assemble, dim3(batch), dim3(kThreads), lds, s, a);
   return launch_status();
 }
