@@ -22,6 +22,10 @@ unless the paper (or the decision being reproduced) fixes another precision:
                        its own ancestors.
 * ``accept``        -- accepted prefix length per path and the best path,
                        Sec. 3.1 Eq. (1) and Sec. 3.5 Eq. (4).
+* ``commit_kv``, ``commit_tokens``
+                    -- committing the winner, Sec. 3.5 and Algorithm 1: its
+                       cache rows moved after the context in depth order, the
+                       emitted tokens, and where the draft-cache replay starts.
 * ``topk``, ``branch_budget``, ``repair_tree``
                     -- the repair tree, Eq. (3), Algorithm 1 and Sec. 3.4:
                        ranked alternatives by a full stable sort, the branch
@@ -37,9 +41,10 @@ from .margins import widen_bf16, as_float32, margins, ufp_select
 from .tree import ancestors, tree_attention
 from .accept import accept
 from .repair import topk, branch_budget, repair_tree
+from .commit import commit_kv, commit_tokens
 
 __all__ = [
     "widen_bf16", "as_float32", "margins", "ufp_select",
     "ancestors", "tree_attention", "accept",
-    "topk", "branch_budget", "repair_tree",
+    "topk", "branch_budget", "repair_tree", "commit_kv", "commit_tokens",
 ]
