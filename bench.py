@@ -10,7 +10,10 @@ already resident in HBM:
 The repair-tree builder (cure_repair_tree: ranked alternatives at the UFPs,
 Eq. 3 branch budget, parent/token assembly) is timed beside the step, on the
 draft-chain rows and UFPs the step's margin pass produced; it is reported
-under `repair_tree` and is not part of `value`.
+under `repair_tree` and is not part of `value`. So is the commit of the
+accepted paths (cure_commit, Sec. 3.5), run on the step's own acceptance
+results over a 32-layer cache of the workload's row shape (Llama-3-8B has 32
+layers), reported under `commit`.
 
 Timing: each input copy's step is captured once as a HIP graph; W warm-up
 replays, then exactly K replays (K steps) bracketed by synchronize() on both
@@ -52,7 +55,10 @@ CSRC = os.path.join(ROOT, "paper_2608_00531_amd", "csrc")
 # Kernel sources behind each call: a stored traffic figure is used only while
 # these files are unchanged since the counters were taken.
 CALL_SOURCES = {"margins": ["margins.hip", "common.hpp"], "attn": ["tree_attn.hip", "common.hpp"],
-                "accept": ["accept.hip", "common.hpp"], "repair": ["repair.hip", "common.hpp"]}
+                "accept": ["accept.hip", "common.hpp"], "repair": ["repair.hip", "common.hpp"],
+                "commit": ["commit.hip", "common.hpp"]}
+# Layers of the cache the commit runs over (a Llama-3-8B-class target).
+COMMIT_LAYERS = 32
 # Eq. 3 parameters of the repair-tree builder: the paper's b_min, b_max, and a
 # margin scale equal to the UFP threshold tau.
 B_MIN, B_MAX = 1, 5
@@ -74,7 +80,7 @@ def parse():
 class Step:
     """Pre-bound C-ABI calls for one input copy (argument marshalling done once)."""
 
-    def __init__(self, pc, torch, w, copy, stream):
+    def __init__(self, pc, torch, w, copy, stream, commit_cache):
         L = pc.lib()
         self.L = L
         dev = torch.device("cuda")
@@ -130,6 +136,17 @@ class Step:
             budget, depth, ctypes.c_float(w.tau), B_MIN, B_MAX, P(copy["suffix"]),
             self.rep_nmax, P(self.rep["parent"]), P(self.rep["token"]),
             P(self.rep["n_nodes"]), P(self.rep["branch_cnt"]), P(self.rws), self.rws.numel(), s)
+        ck, cv = commit_cache
+        self.com = {k: torch.empty(B, **i32) for k in
+                    ("new_ctx_len", "emit_cnt", "replay_start", "status")}
+        self.com["emit"] = torch.empty(B, R + 1, **i32)
+        self.commit_args = (
+            P(ck), P(cv), pc.CURE_BF16 if w.dtype == "bf16" else pc.CURE_F32, ck.shape[0],
+            ck.stride(0), w.hkv, w.d, B, P(copy["kv_off"]), P(copy["ctx_len"]),
+            P(copy["n_nodes"]), P(self.path), P(self.acc["acc_len"]), P(copy["token"]),
+            P(self.acc["bonus"]), w.chain_len, R, P(self.com["new_ctx_len"]),
+            P(self.com["emit"]), P(self.com["emit_cnt"]), P(self.com["replay_start"]),
+            P(self.com["status"]), s)
 
     def margins(self):
         st = self.L.cure_margins(*self.margins_args)
@@ -150,6 +167,11 @@ class Step:
         st = self.L.cure_repair_tree(*self.repair_args)
         if st:
             raise RuntimeError("cure_repair_tree status %d" % st)
+
+    def commit(self):
+        st = self.L.cure_commit(*self.commit_args)
+        if st:
+            raise RuntimeError("cure_commit status %d" % st)
 
     def run(self):
         self.margins()
@@ -222,9 +244,9 @@ def timed_steps(torch, graphs, k, warmup):
 def per_call_times(torch, steps, k):
     """Average GPU duration of each call, from events around every eager launch.
     A spin kernel queued first keeps the host's launch cost off the GPU timeline."""
-    names = ("margins", "attn", "accept", "repair")
+    names = ("margins", "attn", "accept", "repair", "commit")
     n = len(steps)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(k)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(k)]
     torch.cuda.synchronize()
     spin(torch, 25000)
     for i in range(k):
@@ -238,6 +260,8 @@ def per_call_times(torch, steps, k):
         ev[i][3].record()
         s.repair()
         ev[i][4].record()
+        s.commit()
+        ev[i][5].record()
     torch.cuda.synchronize()
     out = {}
     for j, name in enumerate(names):
@@ -282,6 +306,24 @@ def repair_bytes(w, step):
     info = {"rows_ranked": ranked, "branches": branches, "nodes": int(nn.sum()),
             "bytes": total}
     return total, info
+
+
+def commit_bytes(w, step, layers):
+    """Algorithmic bytes of one cure_commit call, from the acceptance results it
+    committed: each moved cache row (path[j] != j) read once and written once,
+    in K and V of every layer, plus the per-sequence sizes, the path and token
+    entries read and the emitted tokens and counters written."""
+    acc = step.acc["acc_len"].cpu().numpy()
+    path = step.path.cpu().numpy()
+    row = w.hkv * w.d * w.elem_bytes()
+    moved = 0
+    for b in range(w.batch):
+        a = max(int(acc[b]), 0)
+        moved += a - sum(1 for j in range(a) if int(path[b][j]) == j)
+    tokens = int(np.maximum(acc, 0).sum())
+    total = (moved * row * 2 * 2 * layers + w.batch * 8 * 4 + tokens * 8
+             + (tokens + w.batch) * 4 + w.batch * 16)
+    return total, {"layers": layers, "rows_moved": moved, "bytes": total}
 
 
 def cpu_baseline(w, algo_bytes, budget_s):
@@ -333,12 +375,18 @@ def main():
     per_copy = sum(base[k].numel() * base[k].element_size() for k in ("logits", "q", "k", "v"))
     ncopy = 1 if args.no_rotate else max(3, math.ceil(ROTATE_BYTES / per_copy))
     copies = [base] + [replicate(torch, base) for _ in range(ncopy - 1)]
+    # The commit's cache: COMMIT_LAYERS layers of the workload's K and V rows.
+    # Its contents do not change the work, so it is left uninitialised.
+    cdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    commit_cache = tuple(torch.empty(COMMIT_LAYERS, w.kv_rows, w.hkv, w.d, dtype=cdt,
+                                     device="cuda") for _ in range(2))
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
-        steps = [Step(pc, torch, w, c, stream.cuda_stream) for c in copies]
+        steps = [Step(pc, torch, w, c, stream.cuda_stream, commit_cache) for c in copies]
         for st in steps:                       # eager reference results, one per copy
             st.run()
             st.repair()
+            st.commit()
         torch.cuda.synchronize()
         ref = [(st.m["top1_idx"].clone(), st.acc["acc_len"].clone(), st.o.clone())
                for st in steps]
@@ -353,15 +401,17 @@ def main():
     assert status == [0] * w.batch, status
     acc_len = steps[0].acc["acc_len"].float().cpu()
     rep_bytes, rep_info = repair_bytes(w, steps[0])
+    com_bytes, com_info = commit_bytes(w, steps[0], COMMIT_LAYERS)
+    assert steps[0].com["status"].cpu().tolist() == [0] * w.batch
 
     call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"],
-                  "repair": rep_bytes}
+                  "repair": rep_bytes, "commit": com_bytes}
     kernels = {}
     for name, us in calls.items():
         gbs = call_bytes[name] / (us * 1e-6) / 1e9
         kernels[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
                          "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
-    step_calls = {k: v for k, v in calls.items() if k != "repair"}
+    step_calls = {k: v for k, v in calls.items() if k not in ("repair", "commit")}
     dom = max(step_calls, key=step_calls.get)
     dom_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
     names = {"margins": "cure_margins (margins_kernel)",
@@ -402,6 +452,12 @@ def main():
                                       "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                       "frac": kernels["repair"]["frac_hbm"],
                                       "traffic": stored_traffic("repair", w.name)}),
+        "commit": dict(com_info, us=round(calls["commit"], 2),
+                       roofline={"bound": "hbm", "kernel": "cure_commit (commit_kernel)",
+                                 "achieved": kernels["commit"]["GB/s"],
+                                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": kernels["commit"]["frac_hbm"],
+                                 "traffic": stored_traffic("commit", w.name)}),
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)

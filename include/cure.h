@@ -13,6 +13,9 @@
  *   cure_repair_tree  the budget-aware repair tree: ranked alternatives at the
  *                   UFPs, the Eq. 3 branch budget and the parent/token arrays
  *                                                       (Sec. 3.3, 3.4, Alg. 1)
+ *   cure_commit     the winning path committed: its cache rows moved after the
+ *                   context in every layer, the emitted tokens, the new context
+ *                   length and the draft-cache replay start   (Sec. 3.5, Alg. 1)
  *
  * Conventions shared by every entry point
  *  - All array arguments are DEVICE pointers (memory the caller allocated with
@@ -233,6 +236,52 @@ cure_status cure_repair_tree(const void* logits, int32_t dtype, int32_t batch, i
                              int32_t n_max, int32_t* parent, int32_t* token, int32_t* n_nodes,
                              int32_t* branch_cnt, void* workspace, size_t workspace_bytes,
                              void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Committing the winning path -- Sec. 3.5 (cache resynchronisation), Alg. 1.
+ *
+ * The accepted tokens become context for the next step. For each sequence b
+ * with a = acc_len[b] accepted nodes and winning path path[b][0 .. a-1] (node
+ * indices, root first, as cure_accept writes them):
+ *   cache       in every layer, cache row kv_off[b] + ctx_len[b] + j takes
+ *               the contents of row kv_off[b] + ctx_len[b] + path[b][j], for
+ *               j < a (tree node n's rows sit at ctx_len + n, as for
+ *               cure_tree_attn), in K and in V. The move is in place; rows from
+ *               ctx_len + a on keep whatever they held.
+ *   new_ctx_len [batch] ctx_len[b] + a
+ *   emit        [batch][n_max + 1] the a accepted tokens token[b][path[b][j]],
+ *               then bonus[b], padded with -1
+ *   emit_cnt    [batch] a + 1
+ *   replay_start [batch] depth of the path's first node numbered >= chain_len
+ *               (a repair node), else a: the emitted tokens from there to a-1
+ *               are the ones to replay into the draft model's cache
+ *   commit_status [batch] CURE_OK, or CURE_ERR_BAD_TREE when the sequence is
+ *               not committable: acc_len < 0 (cure_accept's mark of a malformed
+ *               tree), acc_len > n_nodes, n_nodes outside [0, n_max], a
+ *               negative ctx_len or kv_off, or a path entry outside
+ *               [0, n_nodes) or not above its predecessor. Such a sequence's
+ *               cache is left untouched, new_ctx_len = ctx_len, emit_cnt = 0,
+ *               replay_start = 0 and its emit row is all -1.
+ *
+ * Layout:
+ *   k, v       n_layers caches; layer l's starts at element l * layer_stride
+ *              of k and of v and holds token rows of [hkv][d] dtype elements
+ *              (layer_stride is ignored when n_layers <= 1)
+ *   kv_off [batch] int64, ctx_len, n_nodes, acc_len, bonus [batch] int32,
+ *   path, token [batch][n_max] int32 -- all device memory
+ * Requires hkv * d * sizeof(dtype) to be a multiple of 16 bytes, n_max <= 256,
+ * batch <= 65535. Outputs must not overlap the inputs (new_ctx_len may not be
+ * ctx_len itself: other workgroups still read ctx_len while it is written).
+ * Every cache row kv_off[b] .. kv_off[b] + ctx_len[b] + n_nodes[b] - 1 of
+ * every layer must exist. No workspace.
+ */
+cure_status cure_commit(void* k, void* v, int32_t dtype, int32_t n_layers, int64_t layer_stride,
+                        int32_t hkv, int32_t d, int32_t batch, const int64_t* kv_off,
+                        const int32_t* ctx_len, const int32_t* n_nodes, const int32_t* path,
+                        const int32_t* acc_len, const int32_t* token, const int32_t* bonus,
+                        int32_t chain_len, int32_t n_max, int32_t* new_ctx_len, int32_t* emit,
+                        int32_t* emit_cnt, int32_t* replay_start, int32_t* commit_status,
+                        void* stream);
 
 #ifdef __cplusplus
 }

@@ -50,6 +50,9 @@ _SIGNATURES = {
     "cure_repair_tree": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp,
                                         _i32, _i32, _i32, _f32, _i32, _i32, _vp, _i32,
                                         _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "cure_commit": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, _i32, _i32,
+                                   _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32,
+                                   _vp, _vp, _vp, _vp, _vp, _vp]),
 }
 
 
@@ -265,4 +268,46 @@ def cure_repair_tree(logits, margin, ufp_pos, ufp_cnt, chain_tok, repair_budget,
                             _ptr(out["parent"]), _ptr(out["token"]), _ptr(out["n_nodes"]),
                             _ptr(out["branch_cnt"]), _ptr(ws), wsb, _stream(dev))
     _check(st, "cure_repair_tree")
+    return out
+
+
+def cure_commit(k, v, kv_off, ctx_len, n_nodes, path, acc_len, token, bonus, chain_len,
+                layer_stride=None):
+    """Commit each sequence's winning path, in place.
+
+    k, v: one layer's cache [rows, hkv, d], or n_layers caches [n_layers, rows,
+    hkv, d] (contiguous per layer; layer_stride in elements defaults to the
+    distance between layers). kv_off int64 [batch]; ctx_len, n_nodes, acc_len,
+    bonus int32 [batch]; path, token int32 [batch, n_max] (all on the GPU; path,
+    acc_len and bonus as cure_accept returned them).
+    Returns a dict: new_ctx_len [batch], emit [batch, n_max + 1], emit_cnt,
+    replay_start and status [batch].
+    """
+    _require_cuda(k, v, kv_off, ctx_len, n_nodes, path, acc_len, token, bonus)
+    if k.shape != v.shape or k.dtype != v.dtype or k.dim() not in (3, 4):
+        raise CureError("k and v must have the same shape [n_layers,] rows, hkv, d")
+    if kv_off.dtype != torch.int64 or any(t.dtype != torch.int32 for t in
+                                          (ctx_len, n_nodes, path, acc_len, token, bonus)):
+        raise CureError("kv_off must be int64; the other index arrays int32")
+    n_layers = 1 if k.dim() == 3 else k.shape[0]
+    hkv, d = k.shape[-2], k.shape[-1]
+    for t in (k, v):
+        if tuple(t.stride()[-3:]) != (hkv * d, d, 1):
+            raise CureError("each layer of k and v must be contiguous")
+    if layer_stride is None:
+        layer_stride = 0 if k.dim() == 3 else k.stride(0)
+    if k.dim() == 4 and (k.stride(0) != layer_stride or v.stride(0) != layer_stride):
+        raise CureError("layer_stride does not match the tensors' layer stride")
+    batch, n_max = path.shape
+    dev = k.device
+    i = dict(dtype=torch.int32, device=dev)
+    out = {"new_ctx_len": torch.empty(batch, **i), "emit": torch.empty(batch, n_max + 1, **i),
+           "emit_cnt": torch.empty(batch, **i), "replay_start": torch.empty(batch, **i),
+           "status": torch.empty(batch, **i)}
+    args = [t.contiguous() for t in (kv_off, ctx_len, n_nodes, path, acc_len, token, bonus)]
+    st = lib().cure_commit(_ptr(k), _ptr(v), _dtype_code(k), n_layers, layer_stride, hkv, d,
+                           batch, *[_ptr(t) for t in args], chain_len, n_max,
+                           _ptr(out["new_ctx_len"]), _ptr(out["emit"]), _ptr(out["emit_cnt"]),
+                           _ptr(out["replay_start"]), _ptr(out["status"]), _stream(dev))
+    _check(st, "cure_commit")
     return out

@@ -183,3 +183,32 @@ def test_repair_workspace_size(L):
     assert f(4, 16, 32000, 16, 4) >= 4 * one - 512
     assert f(1, 16, 128256, 16, 4) > one                   # more chunks per row
     assert f(1, 16, 32000, 64, 4) > one                    # more UFP slots
+
+
+def _commit(L, **kw):
+    args = dict(k=1, v=1, dtype=1, n_layers=2, layer_stride=4096, hkv=8, d=128, batch=2,
+                kv_off=1, ctx_len=2, n_nodes=1, path=1, acc_len=1, token=1, bonus=1,
+                chain_len=16, n_max=32, new_ctx_len=3, emit=1, emit_cnt=1, replay_start=1,
+                status=1, stream=None)
+    args.update(kw)
+    return L.cure_commit(*args.values())
+
+
+def test_commit_argument_errors(L):
+    E, U = pc.CURE_ERR_INVALID_ARG, pc.CURE_ERR_UNSUPPORTED
+    assert _commit(L, dtype=3) == E
+    assert _commit(L, batch=-1) == E
+    assert _commit(L, n_layers=-1) == E
+    assert _commit(L, hkv=0) == E
+    assert _commit(L, d=0) == E
+    assert _commit(L, chain_len=-1) == E
+    assert _commit(L, layer_stride=0) == E                 # several layers need a stride
+    assert _commit(L, new_ctx_len=2) == E                  # aliases ctx_len
+    for name in ("kv_off", "ctx_len", "n_nodes", "path", "acc_len", "token", "bonus",
+                 "new_ctx_len", "emit", "emit_cnt", "replay_start", "status", "k", "v"):
+        assert _commit(L, **{name: None}) == E, name
+    assert _commit(L, n_max=257) == U
+    assert _commit(L, hkv=1, d=3, dtype=0) == U            # 12-byte rows
+    assert _commit(L, hkv=1, d=4, dtype=1) == U            # 8-byte rows
+    assert _commit(L, batch=70000) == U
+    assert _commit(L, batch=0) == pc.CURE_OK               # empty: nothing to do
