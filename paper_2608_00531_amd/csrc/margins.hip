@@ -68,6 +68,7 @@ struct Args {
 // without touching memory.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kRsrcWord3 = 0x00020000;   // raw (untyped) 32-bit access, gfx9 family
+constexpr int kNonTemporal = 2;          // cache-policy bit: streaming data, read once
 
 CURE_DEV __amdgpu_buffer_rsrc_t chunk_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
@@ -80,7 +81,7 @@ template <>
 struct Raw8<uint16_t> {
   u32x4 w;
   CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    w = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kNonTemporal);
   }
   static constexpr uint32_t kBytes = 16;
   CURE_DEV void widen(float (&f)[kVec]) const {
@@ -94,8 +95,8 @@ template <>
 struct Raw8<float> {
   u32x4 a, b;
   CURE_DEV void load(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    a = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
-    b = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(off + 16), 0, 0);
+    a = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kNonTemporal);
+    b = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(off + 16), 0, kNonTemporal);
   }
   static constexpr uint32_t kBytes = 32;
   CURE_DEV void widen(float (&f)[kVec]) const {
@@ -178,60 +179,67 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
   float nref = -ref * kLog2e;
 
   int scalar_from = begin;
+  // The lane's two best vectors: their maxima and positions within the chunk
+  // (-1 = none). A lane's first vector is taken as its best even if it is all
+  // -inf, so a lane with data always has one; positions arrive in ascending
+  // order, so strict comparisons keep the first vector attaining each maximum.
+  float bm1 = -INFINITY, bm2 = -INFINITY;
+  int bv1 = -1, bv2 = -1;
+  const int nvec = kVecPath ? (end - begin) / kVec : 0;
   if (kVecPath) {
-    const int nvec = (end - begin) / kVec;
     scalar_from = begin + nvec * kVec;
-    // The lane's two best vectors (index within the chunk, -1 = none).
-    float bm1 = -INFINITY, bm2 = -INFINITY;
-    Raw8<T> kr1, kr2;                    // raw entries of those two vectors
-    int bv1 = -1, bv2 = -1;
     if (nvec > 0) {
       // Lanes past the chunk's last vector read zeros (outside the buffer
       // resource) and ignore them, so every load is unconditional. Two register
       // sets alternate: one step's loads are in flight while the previous step
-      // is processed.
+      // is processed. Steps in which every lane's vectors lie inside the chunk
+      // run without per-vector range checks; only the last step checks.
       const __amdgpu_buffer_rsrc_t rsrc = chunk_rsrc(x + begin, (uint32_t)nvec * Raw8<T>::kBytes);
       const uint32_t lane_off = (uint32_t)tid * Raw8<T>::kBytes;
+      const int full_iters = nvec / (kUnroll * kThreads);
       Raw8<T> ra[kUnroll], rb[kUnroll];
       auto issue = [&](Raw8<T>(&r)[kUnroll], int it) {
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
           r[u].load(rsrc, lane_off + (uint32_t)((it * kUnroll + u) * kThreads) * Raw8<T>::kBytes);
       };
-      auto process = [&](const Raw8<T>(&r)[kUnroll], int it) {
+      auto process = [&](const Raw8<T>(&r)[kUnroll], int it, bool checked) {
+        float f[kUnroll][kVec], m8[kUnroll];
+        float step_max = -INFINITY;
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
           const int v = (it * kUnroll + u) * kThreads + tid;
-          const bool ok = v < nvec;
-          float f[kVec];
-          r[u].widen(f);
-          const float m8 = ok ? max8(f) : -INFINITY;
-          // Best-two-vectors update. The lane's first vector is taken even if it
-          // is all -inf, so a lane with data always has a best vector.
-          const bool c1 = ok && (m8 > bm1 || bv1 < 0);
-          const bool c2 = ok && !c1 && m8 > bm2;
-          bm2 = c1 ? bm1 : (c2 ? m8 : bm2);
+          const bool ok = !checked || v < nvec;
+          r[u].widen(f[u]);
+          m8[u] = ok ? max8(f[u]) : -INFINITY;
+          // Best-two-vectors update (values by max/min, positions by select).
+          const bool c1 = ok && (m8[u] > bm1 || bv1 < 0);
+          const bool c2 = ok && m8[u] > bm2;
           bv2 = c1 ? bv1 : (c2 ? v : bv2);
-          if (c1) kr2 = kr1;
-          if (c2) kr2 = r[u];
-          if (c1) kr1 = r[u];
-          bm1 = c1 ? m8 : bm1;
           bv1 = c1 ? v : bv1;
-          // Log-sum-exp against a lagging reference, moved only on large jumps.
-          const bool resc = m8 > ref + kRescaleAt;
-          if (__builtin_expect(__ballot(resc) != 0, 0)) {
-            if (resc) {
-              sum *= fast_exp2((ref - m8) * kLog2e);
-              ref = m8;
-              nref = -ref * kLog2e;
-            }
+          bm2 = fmaxf(bm2, fminf(m8[u], bm1));
+          bm1 = fmaxf(bm1, m8[u]);
+          step_max = fmaxf(step_max, m8[u]);
+        }
+        // Log-sum-exp against a lagging reference, moved only on large jumps
+        // (checked once per step, before the step's terms are added).
+        const bool resc = step_max > ref + kRescaleAt;
+        if (__builtin_expect(__ballot(resc) != 0, 0)) {
+          if (resc) {
+            sum *= fast_exp2((ref - step_max) * kLog2e);
+            ref = step_max;
+            nref = -ref * kLog2e;
           }
-          if (ok) {
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int v = (it * kUnroll + u) * kThreads + tid;
+          if (!checked || v < nvec) {
             float s0 = 0.f, s1 = 0.f;
 #pragma unroll
             for (int j = 0; j < kVec; j += 2) {
-              s0 += fast_exp2(fmaf(f[j], kLog2e, nref));
-              s1 += fast_exp2(fmaf(f[j + 1], kLog2e, nref));
+              s0 += fast_exp2(fmaf(f[u][j], kLog2e, nref));
+              s1 += fast_exp2(fmaf(f[u][j + 1], kLog2e, nref));
             }
             sum += s0 + s1;
           }
@@ -240,24 +248,19 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
       // Prefetches past the last step fall outside the resource and read zeros,
       // so they need no guard and the waits before each step stay partial.
       issue(ra, 0);
-      for (int it = 0; it < a.iters; it += 2) {
+      int it = 0;
+      for (; it + 1 < full_iters; it += 2) {
         issue(rb, it + 1);
-        process(ra, it);
-        if (it + 1 >= a.iters) break;
+        process(ra, it, false);
         issue(ra, it + 2);
-        process(rb, it + 1);
+        process(rb, it + 1, false);
       }
-    }
-    // Exact top-2 over the entries of the lane's two best vectors.
-    if (bv1 >= 0) {
-      float f[kVec];
-      kr1.widen(f);
-#pragma unroll
-      for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + bv1 * kVec + j);
-      if (bv2 >= 0) {
-        kr2.widen(f);
-#pragma unroll
-        for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + bv2 * kVec + j);
+      // At most two steps remain (ra holds step `it`): one full or checked
+      // step, then possibly a checked one.
+      if (it < a.iters) {
+        issue(rb, it + 1);
+        process(ra, it, it >= full_iters);
+        if (it + 1 < a.iters) process(rb, it + 1, true);
       }
     }
   }
@@ -272,9 +275,33 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
     sum += fast_exp2(fmaf(xv, kLog2e, nref));
   }
 
+  // The wave's top-2 entries lie in its two best vectors (by maximum
+  // descending, position ascending) together with the lanes' scalar-tail
+  // entries. The lanes' vector records are merged first (positions as indices;
+  // "none" is (-inf, INT32_MAX), which every real vector beats) and only those
+  // two vectors are reloaded, by lanes 0 and 1: two 16-byte reads per wave
+  // instead of one scattered read per lane. The log-sum-exp reduction runs
+  // while they are in flight.
+  const int lane = tid & (kWave - 1);
+  int mine = INT32_MAX;
+  Raw8<T> k;
+  if (kVecPath) {
+    const Top2 bv = top2_wave_reduce(Top2{bm1, bm2, bv1 < 0 ? INT32_MAX : bv1,
+                                          bv2 < 0 ? INT32_MAX : bv2});
+    mine = lane == 0 ? bv.i1 : (lane == 1 ? bv.i2 : INT32_MAX);
+    if (mine != INT32_MAX)
+      k.load(chunk_rsrc(x + begin, (uint32_t)nvec * Raw8<T>::kBytes), (uint32_t)mine * Raw8<T>::kBytes);
+  }
+  Lse s = lse_wave_reduce(Lse{ref, sum});
+  if (kVecPath && mine != INT32_MAX) {
+    float f[kVec];
+    k.widen(f);
+#pragma unroll
+    for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + mine * kVec + j);
+  }
+
   // Workgroup reduction.
   t = top2_wave_reduce(t);
-  Lse s = lse_wave_reduce(Lse{ref, sum});
   const int wave = tid / kWave;
   if ((tid & (kWave - 1)) == 0) { s_top[wave] = t; s_lse[wave] = s; }
   __syncthreads();

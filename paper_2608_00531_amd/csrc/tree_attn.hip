@@ -330,7 +330,7 @@ CURE_DEV uint32_t lds_addr(const void* p) {
 // land at lds_base + 16 * i (lds_base travels in M0). Out-of-range offsets
 // read as zero.
 CURE_DEV void dma16(uint32_t lds_base, uint32_t voff, i32x4 rsrc) {
-  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
                :
                : "v"(voff), "s"(rsrc), "{m0}"(lds_base)
                : "memory");
