@@ -74,6 +74,13 @@ def parse():
                    help="approximate CPU time spent on the oracle baseline (0 = skip)")
     p.add_argument("--no-rotate", action="store_true",
                    help="reuse one input copy (cache-warm numbers; never the headline)")
+    p.add_argument("--sweep", action="store_true",
+                   help="acceptance-compute trade-off over the repair budgets 0-64 at "
+                        "batch 8, context 8192: one line per budget, then the rate model")
+    p.add_argument("--layers", type=int, default=32,
+                   help="target layers in the sweep's verification cost model")
+    p.add_argument("--accept-trees", type=int, default=2048,
+                   help="seeded trees per budget for the sweep's mean accepted length")
     return p.parse_args()
 
 
@@ -356,19 +363,9 @@ def cpu_baseline(w, algo_bytes, budget_s):
                       "threads=%d, sorts single-threaded" % (reps, w.name, threads)}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-    import torch
-    import paper_2608_00531_amd as pc
-    from synth import preset, algorithmic_bytes
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    w = preset(args.workload)
+def measure(w, args, torch, pc):
+    """Times one workload's step (and the calls beside it); returns the JSON line."""
+    from synth import algorithmic_bytes
     ab = algorithmic_bytes(w)
     step_bytes = ab["attention"] + ab["margins"] + ab["accept"]
     base = upload_copy(torch, w)
@@ -461,7 +458,100 @@ def main():
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)
-    print(json.dumps(line), flush=True)
+    return line
+
+SWEEP_BUDGETS = (0, 8, 16, 32, 64)
+# Parameters of a Llama-3-8B-class target for the sweep's cost model: its
+# weights are streamed once per verification pass.
+TARGET_PARAMS = 8.03e9
+TARGET_BYTES_PER_PARAM = 2
+
+
+def mean_accepted(pc, torch, budget, n_trees, seed):
+    """Mean accepted length E[a] (and E[a] + 1 tokens per step) over n_trees
+    seeded trees of the sweep's shape (chain 16, depth-4 branches at seeded
+    positions), against the synthetic target that agrees with each node with
+    probability 0.8 i.i.d., computed by cure_accept on the GPU."""
+    from synth import make_workload
+    w = make_workload("accept_sample", dtype="f32", batch=n_trees, hq=1, hkv=1, d=4, vocab=64,
+                      ctx_lens=[1] * n_trees, chain_len=16, n_ufp=budget // 4, branch_depth=4,
+                      seed=700 + seed, p_agree=0.8)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    out = pc.cure_accept(t(w.parent), t(w.token), t(w.tgt_planted), t(w.root_tgt), t(w.n_nodes),
+                         w.chain_len)
+    acc = out["acc_len"].float().cpu().numpy()
+    assert acc.min() >= 0
+    return float(acc.mean()), float(acc.std() / math.sqrt(len(acc))), float(out["resync"].float().mean())
+
+
+def sweep(args, torch, pc):
+    """Acceptance-compute trade-off (Sec. 3.1's rate model): for each repair
+    budget, the measured verify step and the mean accepted length, then the
+    modelled generation rate (E[a] + 1) / (C_d + C_v(N)) with
+
+      C_v(N) = layers x t_attn(N) + t_margins(N) + t_accept + t_weights,
+
+    t_attn, t_margins, t_accept measured here for the budget's tree (N nodes
+    per sequence), t_weights = the target's weight bytes at the measured margin
+    pass bandwidth (one streaming read of the weights per verification pass),
+    and a synthetic draft cost C_d given as multiples of t_weights (the paper's
+    drafter is a target-sized block-parallel model: one forward, C_d ~ t_weights).
+    The budget that maximises the rate is reported per C_d."""
+    from synth import preset
+    rows = []
+    for budget in SWEEP_BUDGETS:
+        w = preset("llama3_8b_ctx8k_b8_budget%d" % budget)
+        line = measure(w, args, torch, pc)
+        ea, ea_se, resync = mean_accepted(pc, torch, budget, args.accept_trees, budget)
+        line["sweep"] = {"budget": budget, "tree_nodes": int(w.n_nodes.max()),
+                         "mean_accepted": round(ea, 4), "mean_accepted_se": round(ea_se, 4),
+                         "resync_rate": round(resync, 4), "accept_trees": args.accept_trees}
+        print(json.dumps(line), flush=True)
+        rows.append((budget, w, line, ea))
+    # Weight streaming at the bandwidth the margin pass reached on this GPU.
+    bw = max(r[2]["kernels"]["margins"]["GB/s"] for r in rows) * 1e9
+    t_weights = TARGET_PARAMS * TARGET_BYTES_PER_PARAM / bw * 1e6
+    table = []
+    for budget, w, line, ea in rows:
+        k = line["kernels"]
+        cv = args.layers * k["attn"]["us"] + k["margins"]["us"] + k["accept"]["us"] + t_weights
+        table.append({"budget": budget, "tree_nodes": int(w.n_nodes.max()),
+                      "mean_accepted": round(ea, 4), "attn_us": k["attn"]["us"],
+                      "c_v_us": round(cv, 1)})
+    best = {}
+    for ratio in (0.25, 0.5, 1.0, 2.0):
+        cd = ratio * t_weights
+        rates = []
+        for row in table:
+            rate = (row["mean_accepted"] + 1) * 8 / ((cd + row["c_v_us"]) * 1e-6)
+            row["tokens_per_s_cd%.2g" % ratio] = round(rate, 1)
+            rates.append((rate, row["budget"]))
+        top = max(rates)
+        best["cd_%.2g_x_weights" % ratio] = {"budget": top[1], "tokens_per_s": round(top[0], 1),
+                                             "gain_vs_budget0": round(top[0] / rates[0][0], 4)}
+    print(json.dumps({"sweep_summary": {
+        "model": "rate = (E[a] + 1) * batch / (C_d + C_v(N)); C_v = layers * attn + margins + "
+                 "accept + weight streaming; C_d synthetic, in multiples of the weight stream",
+        "layers": args.layers, "batch": 8, "t_weights_us": round(t_weights, 1),
+        "weights_gbps": round(bw / 1e9, 1), "rows": table, "best_budget": best}}), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_00531_amd as pc
+    from synth import preset
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    if args.sweep:
+        sweep(args, torch, pc)
+        return
+    print(json.dumps(measure(preset(args.workload), args, torch, pc)), flush=True)
 
 
 if __name__ == "__main__":
