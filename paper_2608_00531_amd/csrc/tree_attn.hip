@@ -37,6 +37,7 @@ namespace {
 
 constexpr int kTile = 64;            // tokens per K/V tile
 constexpr int kStages = 2;           // K/V tile buffers in the MFMA kernel's LDS ring
+constexpr int kMaxGridY = 65535;     // largest grid y (the split index)
 constexpr int kMinTps = 256;         // tokens per split, at least
 constexpr int kAncWords = CURE_MAX_TREE_NODES / 64;
 
@@ -158,9 +159,9 @@ __global__ __launch_bounds__(256) void tree_attn_valu(Args a) {
   __shared__ float s_p[kValuWaves][kValuRowsPerWave][kTile];
 
   const int b = blockIdx.z;
-  const int hk = blockIdx.y % a.hkv;
-  const int rb = blockIdx.y / a.hkv;
-  const int s = blockIdx.x;
+  const int hk = blockIdx.x % a.hkv;
+  const int rb = blockIdx.x / a.hkv;
+  const int s = blockIdx.y;
   const int N = min(a.n_nodes[b], a.n_max);
   const int L = a.ctx_len[b];
   const int T = L + N;
@@ -398,9 +399,9 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
   __shared__ __attribute__((aligned(1024))) unsigned char s_v[NBUF][G::kTileBytes];
 
   const int b = blockIdx.z;
-  const int hk = blockIdx.y % a.hkv;
-  const int rb = blockIdx.y / a.hkv;
-  const int s = blockIdx.x;
+  const int hk = blockIdx.x % a.hkv;
+  const int rb = blockIdx.x / a.hkv;
+  const int s = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, col = lane & 31;
 
@@ -712,9 +713,9 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
   __shared__ __attribute__((aligned(1024))) unsigned char s_v[2][G::kTileBytes];
 
   const int b = blockIdx.z;
-  const int hk = blockIdx.y % a.hkv;
-  const int rb = blockIdx.y / a.hkv;
-  const int s = blockIdx.x;
+  const int hk = blockIdx.x % a.hkv;
+  const int rb = blockIdx.x / a.hkv;
+  const int s = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
 
@@ -1137,6 +1138,8 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
       tps = z * kTile;
     }
   }
+  // Splits index the grid's y dimension (at most kMaxGridY).
+  tps = std::max<int64_t>(tps, round_tile((t_max + kMaxGridY - 1) / kMaxGridY));
   p.tps = (int)std::min<int64_t>(tps, INT32_MAX / 2);
   p.max_splits = t_max > 0 ? (int)((t_max + p.tps - 1) / p.tps) : 0;
   return p;
@@ -1245,7 +1248,10 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   }
 
   hipStream_t st = as_stream(stream);
-  const dim3 grid(p.max_splits, hkv * p.row_blocks, batch);
+  // KV heads (and row blocks) vary fastest: consecutive workgroups, which the
+  // dispatcher spreads over the XCDs and starts together, read the heads of
+  // the same token range, so concurrent reads cover whole cache rows.
+  const dim3 grid(hkv * p.row_blocks, p.max_splits, batch);
   if (p.rows16) {
     if (d == 128) {
       if (p.nw == 8) hipLaunchKernelGGL((tree_attn_m16<128, 8>), grid, dim3(512), 0, st, a);
