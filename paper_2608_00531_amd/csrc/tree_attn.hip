@@ -952,13 +952,14 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   constexpr int kLanesPerSplit = D / 4;
   constexpr int kSplitsPerLoad = kWave / kLanesPerSplit;
   constexpr int kSplitsPerBatch = kSplitsPerLoad * NB;
+  // Grid (heads / 4, n_max, batch): the row's coordinates come straight from
+  // the block index (no 64-bit divisions).
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;
-  const int64_t nrows = (int64_t)batch * a.n_max * a.hq;
-  if (rowid >= nrows) return;
-  const int head = (int)(rowid % a.hq);
-  const int n = (int)((rowid / a.hq) % a.n_max);
-  const int b = (int)(rowid / ((int64_t)a.hq * a.n_max));
+  const int head = blockIdx.x * 4 + wave;
+  const int n = blockIdx.y;
+  const int b = blockIdx.z;
+  (void)batch;
+  if (head >= a.hq) return;
   const int64_t p0 = part_index(a, b, head, n, 0);
   const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
   const int col = (lane % kLanesPerSplit) * 4;      // its four output columns
@@ -1273,8 +1274,7 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   }
   if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
   if (p.max_splits > 1) {
-    const int64_t nrows = (int64_t)batch * n_max * hq;
-    const dim3 mgrid((unsigned)((nrows + 3) / 4));
+    const dim3 mgrid((unsigned)((hq + 3) / 4), (unsigned)n_max, (unsigned)batch);
     const int per_load = 256 / d;                       // splits per merge load
     const int nb = p.max_splits <= 2 * per_load ? 2 : p.max_splits <= 4 * per_load ? 4 : 8;
     if (d == 128) {
