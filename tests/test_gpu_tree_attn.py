@@ -176,6 +176,26 @@ def test_long_context_full_size_sampled():
     check_attn(w, o, lse, ref_o, ref_l, sample=sample)
 
 
+def test_largest_sweep_tree_full_size_sampled():
+    # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, two row blocks of
+    # the 32-row kernel, in the launch configuration the budget sweep times.
+    say("attn llama3_8b_ctx8k_b8_budget64 sampled")
+    with Timer("generate"):
+        w = preset("llama3_8b_ctx8k_b8_budget64")
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK] * w.batch
+    rng = np.random.default_rng(1)
+    sample = [(b, int(n)) for b in range(w.batch) for n in rng.choice(80, 2, replace=False)]
+    # Chain ends, the first node of the second row block (rows 256+ are nodes
+    # 64+ with 4 query heads per kv-head) and the last node.
+    sample += [(0, 0), (1, 15), (2, 63), (3, 64), (7, 79)]
+    with Timer("oracle"):
+        ref_o, ref_l = oracle_attn(w, sample=sample)
+    check_attn(w, o, lse, ref_o, ref_l, sample=sample)
+
+
 def test_nonpositive_scale_takes_the_general_path():
     say("attn negative scale")
     w = make_workload("n", batch=2, hq=8, hkv=2, ctx_lens=[300, 71], chain_len=8, n_ufp=2,
