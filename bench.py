@@ -29,6 +29,8 @@ The printed JSON line's `value` is the step's algorithmic bytes over its time
 `traffic` is the calibrated FETCH_SIZE + WRITE_SIZE bytes per call stored in
 profiles/traffic_<workload>.json, or null when that file is missing or the
 call's kernel sources have changed since the counters were taken.
+`read_ceiling` is the rate of a plain streaming read of a 1 GiB buffer
+(cure_read_ceiling), the practical ceiling for the roofline fractions.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload
 on this host.
 """
@@ -315,6 +317,26 @@ def repair_bytes(w, step):
     return total, info
 
 
+def read_ceiling(torch, pc, reps=20, nbytes=1 << 30):
+    """The practical HBM read rate on this GPU: cure_read_ceiling (a plain
+    non-temporal streaming read, one workgroup per 256 KB) over a 1 GiB buffer,
+    four times the last-level cache, median of `reps` event-timed reads."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    pc.cure_read_ceiling(buf)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(reps):
+        pc.cure_read_ceiling(buf)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    us = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(reps))[reps // 2]
+    gbs = nbytes / (us * 1e-6) / 1e9
+    del buf
+    return {"GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "bytes": nbytes,
+            "kernel": "cure_read_ceiling (read_ceiling_kernel)"}
+
+
 def commit_bytes(w, step, layers):
     """Algorithmic bytes of one cure_commit call, from the acceptance results it
     committed: each moved cache row (path[j] != j) read once and written once,
@@ -456,6 +478,7 @@ def measure(w, args, torch, pc):
                                  "frac": kernels["commit"]["frac_hbm"],
                                  "traffic": stored_traffic("commit", w.name)}),
     }
+    line["read_ceiling"] = read_ceiling(torch, pc)
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)
     return line

@@ -283,6 +283,20 @@ cure_status cure_commit(void* k, void* v, int32_t dtype, int32_t n_layers, int64
                         int32_t* emit_cnt, int32_t* replay_start, int32_t* commit_status,
                         void* stream);
 
+/* ------------------------------------------------------------------------- */
+/* Read ceiling -- a measurement aid, not a step of the method.
+ *
+ * Streams `bytes` of device memory (a multiple of 16) the way the margin pass
+ * streams its rows: one workgroup per 256 KB chunk, 16-byte non-temporal
+ * loads. Writes the XOR of each chunk's 32-bit words to chunk_xor[i] (device,
+ * cure_read_ceiling_chunks(bytes) entries), so the read is needed and can be
+ * checked. Its time is the practical HBM read rate the hot path's bandwidth is
+ * compared against.
+ */
+size_t cure_read_ceiling_chunks(size_t bytes);
+
+cure_status cure_read_ceiling(const void* buf, size_t bytes, uint32_t* chunk_xor, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,7 +14,7 @@ LIB_DIR = os.path.join(PKG, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libcure.so")
 INCLUDE = os.path.join(ROOT, "include")
 
-SOURCES = ["api.cpp", "margins.hip", "accept.hip", "tree_attn.hip", "repair.hip", "commit.hip"]
+SOURCES = ["api.cpp", "margins.hip", "accept.hip", "tree_attn.hip", "repair.hip", "commit.hip", "ceiling.hip"]
 
 # Packed fp32 arithmetic is disabled for all device code.
 HIPCC_FLAGS = [

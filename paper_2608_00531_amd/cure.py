@@ -50,6 +50,8 @@ _SIGNATURES = {
     "cure_repair_tree": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64, _vp, _vp, _vp, _vp,
                                         _i32, _i32, _i32, _f32, _i32, _i32, _vp, _i32,
                                         _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "cure_read_ceiling_chunks": (_sz, [_sz]),
+    "cure_read_ceiling": (ctypes.c_int, [_vp, _sz, _vp, _vp]),
     "cure_commit": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i64, _i32, _i32, _i32,
                                    _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32,
                                    _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -310,4 +312,19 @@ def cure_commit(k, v, kv_off, ctx_len, n_nodes, path, acc_len, token, bonus, cha
                            _ptr(out["new_ctx_len"]), _ptr(out["emit"]), _ptr(out["emit_cnt"]),
                            _ptr(out["replay_start"]), _ptr(out["status"]), _stream(dev))
     _check(st, "cure_commit")
+    return out
+
+
+def cure_read_ceiling(buf):
+    """Streams a contiguous GPU tensor (size a multiple of 16 bytes) once; returns
+    the per-256-KB-chunk XOR of its 32-bit words (int32 tensor)."""
+    _require_cuda(buf)
+    if not buf.is_contiguous():
+        raise CureError("the buffer must be contiguous")
+    nbytes = buf.numel() * buf.element_size()
+    L = lib()
+    out = torch.empty(max(int(L.cure_read_ceiling_chunks(nbytes)), 1), dtype=torch.int32,
+                      device=buf.device)
+    _check(L.cure_read_ceiling(_ptr(buf), nbytes, _ptr(out), _stream(buf.device)),
+           "cure_read_ceiling")
     return out

@@ -212,3 +212,14 @@ def test_commit_argument_errors(L):
     assert _commit(L, hkv=1, d=4, dtype=1) == U            # 8-byte rows
     assert _commit(L, batch=70000) == U
     assert _commit(L, batch=0) == pc.CURE_OK               # empty: nothing to do
+
+
+def test_read_ceiling_argument_errors(L):
+    assert L.cure_read_ceiling_chunks(0) == 0
+    assert L.cure_read_ceiling_chunks(1) == 1
+    assert L.cure_read_ceiling_chunks(256 << 10) == 1
+    assert L.cure_read_ceiling_chunks((256 << 10) + 16) == 2
+    assert L.cure_read_ceiling(None, 0, None, None) == pc.CURE_OK      # nothing to read
+    assert L.cure_read_ceiling(None, 64, 1, None) == pc.CURE_ERR_INVALID_ARG
+    assert L.cure_read_ceiling(1, 64, None, None) == pc.CURE_ERR_INVALID_ARG
+    assert L.cure_read_ceiling(1, 60, 1, None) == pc.CURE_ERR_INVALID_ARG  # not 16-byte multiple
