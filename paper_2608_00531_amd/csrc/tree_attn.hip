@@ -711,6 +711,10 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
   constexpr int kKSteps = D / 32;                  // k-steps for Q K^T
   constexpr int kDBlk = D / 16;                    // 16-column blocks of O^T
   constexpr int kDmaPerWave = G::kBlocks / NW;     // DMA blocks per wave per tensor
+  constexpr int kKFrags = 4 * kKSteps;             // K operand fragments per tile
+  constexpr int kVFrags = 2 * kDBlk;               // V^T operand fragments per tile
+  constexpr int kAheadK = 4;                       // K reads in flight ahead of their MFMA
+  constexpr int kAheadV = 4;                       // V^T reads in flight ahead of their MFMA
   static_assert(G::kBlocks % NW == 0, "tile must split evenly across waves");
 
   __shared__ int s_parent[CURE_MAX_TREE_NODES];
@@ -839,18 +843,33 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
     const unsigned char* kt = s_k[buf];
     const unsigned char* vt = s_v[buf];
 
-    // Scores: four 16-token blocks, each a chain of kKSteps MFMAs.
+    // Scores: four 16-token blocks, each a chain of kKSteps MFMAs. The K
+    // operand reads run kAheadK fragments ahead of the MFMA that takes them,
+    // so LDS latency overlaps the matrix core instead of stalling each MFMA.
     f32x4 sacc[4];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) sacc[tb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    Pack8 kf[kKFrags];
 #pragma unroll
-    for (int ks = 0; ks < kKSteps; ++ks)
+    for (int i = 0; i < kAheadK; ++i) kf[i].u = *reinterpret_cast<const uint4*>(kt + k_off[i & 3][i >> 2]);
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        Pack8 ka;
-        ka.u = *reinterpret_cast<const uint4*>(kt + k_off[tb][ks]);
-        sacc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka.v, qreg[ks], sacc[tb], 0, 0, 0);
+    for (int i = 0; i < kKFrags; ++i) {
+      if (i + kAheadK < kKFrags) {
+        const int j = i + kAheadK;
+        kf[j].u = *reinterpret_cast<const uint4*>(kt + k_off[j & 3][j >> 2]);
       }
+      sacc[i & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[i].v, qreg[i >> 2], sacc[i & 3], 0, 0, 0);
+    }
+    // Left alone, the scheduler sinks each read back next to its MFMA; pin the
+    // order: kAheadK reads, then alternate one MFMA (0x008) and one LDS read
+    // (0x100), then the last kAheadK MFMAs.
+    __builtin_amdgcn_sched_group_barrier(0x100, kAheadK, 0);
+#pragma unroll
+    for (int i = 0; i < kKFrags - kAheadK; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAheadK, 0);
     if (t0 + kTile > L) {
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb)
@@ -878,6 +897,19 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
         m_run = m_tile;
       }
     }
+    // V^T fragment i: k-step i / kDBlk, column block i % kDBlk. The first
+    // kAheadV go out before the exponentials, which then hide their latency.
+    Pack8 vf[kVFrags];
+    auto load_v = [&](Pack8& f, int i) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row = 32 * (i / kDBlk) + 16 * h + v_row;
+        const int byte = G::offset(row, 2 * (i % kDBlk) + v_chunk) + v_byte;
+        f.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vt + byte));
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
     const float nm = m_run == -INFINITY ? 0.f : -m_run;
     bf16x8 pb[2];                                  // k-steps kt = 0, 1 (blocks 2 kt, 2 kt + 1)
     float l0 = 0.f, l1 = 0.f;
@@ -896,18 +928,11 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
     l_run += l0 + l1;
 
 #pragma unroll
-    for (int kt2 = 0; kt2 < 2; ++kt2)
-#pragma unroll
-      for (int db = 0; db < kDBlk; ++db) {
-        Pack8 va;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int row = 32 * kt2 + 16 * h + v_row;
-          const int byte = G::offset(row, 2 * db + v_chunk) + v_byte;
-          va.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vt + byte));
-        }
-        oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va.v, pb[kt2], oacc[db], 0, 0, 0);
-      }
+    for (int i = 0; i < kVFrags; ++i) {
+      if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
+      oacc[i % kDBlk] =
+          __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[i].v, pb[i / kDBlk], oacc[i % kDBlk], 0, 0, 0);
+    }
   }
 
   __builtin_amdgcn_s_waitcnt(0);          // the trailing out-of-range DMA lands before exit
