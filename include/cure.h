@@ -138,6 +138,11 @@ cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch, int32
  * kv_split: 0 = automatic, else the number of context splits per sequence.
  * flags: CURE_ATTN_FORCE_VALU or 0.
  * workspace: cure_tree_attn_workspace_size(...) bytes for the same arguments.
+ *   It holds each context split's fp32 partial rows and their log-sum-exps;
+ *   the splits are combined by a log-sum-exp merge.
+ * Alignment (else CURE_ERR_INVALID_ARG): workspace 16 bytes; on the bf16
+ * matrix-core path (bf16 inputs, d 64 or 128, scale > 0, no FORCE_VALU) also
+ * q, k, v 16 bytes and o 8 bytes (bf16 out) or 16 bytes (fp32 out).
  */
 size_t cure_tree_attn_workspace_size(int32_t batch, int32_t hq, int32_t hkv, int32_t d,
                                      int32_t n_max, const int32_t* host_ctx_len,

@@ -1279,6 +1279,8 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
     if (a.out_bf16 ? reinterpret_cast<uintptr_t>(o) % 8 : reinterpret_cast<uintptr_t>(o) % 16)
       return CURE_ERR_INVALID_ARG;
   }
+  // Split partials are written and read as 16-byte vectors.
+  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return CURE_ERR_INVALID_ARG;
 
   hipStream_t st = as_stream(stream);
   // KV heads (and row blocks) vary fastest: consecutive workgroups, which the

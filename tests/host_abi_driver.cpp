@@ -91,6 +91,13 @@ int main() {
   expect(attn(1, 128, 32, 30, 8, nullptr), CURE_ERR_INVALID_ARG, "attn gqa");
   expect(attn(1, 128, 16, 32, 8, nullptr), CURE_ERR_INVALID_ARG, "attn nodes > n_max");
   expect(attn(1, 128, 32, 32, 8, nullptr), CURE_ERR_WORKSPACE, "attn workspace");
+  void* const P4 = reinterpret_cast<void*>(uintptr_t(0x1004));
+  expect((int)cure_tree_attn(P, P, P, P4, F, 1, 1, 4, 32, 8, 128, 0.125f, I64, I, I, I, 32,
+                             ctx.data(), nn.data(), 0, 0u, I, P, size_t(1) << 40, nullptr),
+         CURE_ERR_INVALID_ARG, "attn o alignment");
+  expect((int)cure_tree_attn(P, P, P, P, F, 1, 1, 4, 32, 8, 128, 0.125f, I64, I, I, I, 32,
+                             ctx.data(), nn.data(), 0, 0u, I, P4, size_t(1) << 40, nullptr),
+         CURE_ERR_INVALID_ARG, "attn workspace alignment");
 
   // Acceptance walk, repair tree, commit, read ceiling: argument errors.
   expect((int)cure_accept(I, I, I, I, I, 4, 2, 300, I, I, I, I, I, nullptr), CURE_ERR_UNSUPPORTED,

@@ -108,6 +108,20 @@ def test_tree_attn_argument_errors(L):
     assert _attn(L, batch=0) == pc.CURE_OK
 
 
+def test_tree_attn_alignment_errors(L):
+    # The matrix-core path (bf16, d 64) moves q, k, v and o as vectors: o must
+    # be 8-byte (bf16) or 16-byte (fp32) aligned; split partials need a
+    # 16-byte aligned workspace on every path.
+    ok = dict(q=4096, k=4096, v=4096)
+    assert _attn(L, o=4100, **ok) == pc.CURE_ERR_INVALID_ARG                   # bf16 out, 4 mod 8
+    assert _attn(L, o=4104, out_dtype=pc.CURE_F32, **ok) == pc.CURE_ERR_INVALID_ARG
+    assert _attn(L, q=4104, k=4096, v=4096, o=4096) == pc.CURE_ERR_INVALID_ARG  # MFMA operands
+    # 1000 context rows in 2 splits need partials, so the workspace is checked.
+    ctx = np.array([1000], np.int32)
+    assert _attn(L, o=4096, kv_split=2, workspace=4104, ws_bytes=1 << 24,
+                 host_ctx_len=ctx.ctypes.data_as(ctypes.c_void_p), **ok) == pc.CURE_ERR_INVALID_ARG
+
+
 def test_tree_attn_workspace_size_tracks_splits(L):
     ctx = np.array([32768] * 4, np.int32)
     nn = np.array([32] * 4, np.int32)
