@@ -10,14 +10,15 @@
 // of every tree node, packed node-major. Only tiles that reach the tree rows
 // at the tail of the sequence apply the ancestor bitmask.
 //
-// Two kernels compute a split:
-//  * tree_attn_mfma: bf16, head dim 64/128, scale > 0. Scores are formed
-//    transposed, S^T = K Q^T, and the output as O^T = V^T P^T with 32x32x16
-//    bf16 MFMAs, so each lane owns one query row and the online softmax needs
-//    no cross-lane traffic beyond one exchange between the two half-waves.
-//    K/V tiles arrive in LDS by DMA; V is read back transposed by the LDS
-//    transpose-read instruction in exactly the token order the score MFMA
-//    leaves P in registers.
+// Three kernels compute a split:
+//  * tree_attn_m16: bf16, scale > 0, head dim 128 (any row count, in
+//    balanced row blocks of up to 256 rows) or 64 (up to 128 rows). Scores
+//    are formed transposed, S^T = K Q^T, and the output as O^T = V^T P^T with
+//    16x16x32 bf16 MFMAs, 16 query rows per wave. K/V tiles arrive in LDS by
+//    DMA; V is read back transposed by the LDS transpose-read instruction in
+//    exactly the token order the score MFMA leaves P in registers.
+//  * tree_attn_mfma: the same scheme with 32x32x16 MFMAs and 32 rows per
+//    wave, for head dim 64 beyond 128 rows.
 //  * tree_attn_valu: fp32 or bf16, any supported shape and scale; plain vector
 //    ALU code.
 // A split writes normalised partial O and its log-sum-exp; attn_merge combines
@@ -689,8 +690,12 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 //
 // Same tile stream, LDS layout, tree mask and online softmax as the 32-row
 // kernel above, at half the registers per wave, so that two 8-wave
-// workgroups (four waves per SIMD) share a CU and larger row counts (up to
-// 256) fit one workgroup with the rows spread evenly over the SIMDs.
+// workgroups (four waves per SIMD) share a CU, and row blocks of up to 256
+// rows fit one 16-wave workgroup with the rows spread evenly over the SIMDs.
+// Wider trees take several row blocks of equal size (a multiple of 16 rows).
+// The row blocks of one kv-head and split are hkv workgroup ids apart: with
+// hkv a multiple of 8 the dispatcher, which deals workgroups to the 8 XCDs in
+// turn, puts them on the same XCD, where they share its L2 for the K/V stream.
 //
 // Lane l = 16 g + c (c = l % 16, g = l / 16) owns query row c of its wave.
 //   S^T = K Q^T, per 16-token block tb and 32-wide k-step ks:
@@ -797,10 +802,12 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
   };
   dma_tile(0, begin);
 
-  const bool row_ok = R < rows;
+  // A row block may hold fewer rows than the workgroup has row waves.
+  const bool own = wave * 16 < a.rows_per_wg;
+  const bool row_ok = own && R < rows;
   const int n = row_ok ? R / a.group : 0;
   const int head = hk * a.group + (row_ok ? R % a.group : 0);
-  const bool wave_active = rb * a.rows_per_wg + wave * 16 < rows;
+  const bool wave_active = own && rb * a.rows_per_wg + wave * 16 < rows;
 
   // LDS byte offsets of this lane's operands inside a tile.
   int k_off[4][kKSteps];                           // K: row tb*16 + c, chunk 4 ks + g
@@ -1109,14 +1116,17 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   p.mfma = mfma;
   const int group = hq / hkv;
   const int rows = n_max * group;
-  // Up to 256 rows per kv-head (128 at head dim 64) the 16-row kernel takes
-  // them in one workgroup: 8 waves for up to 128 rows, else 16. Beyond that
-  // the 32-row kernel's 8-wave row blocks (256 rows each) measured faster.
-  p.rows16 = mfma && rows <= (d == 128 ? 256 : 128);
+  // Head dim 128: the 16-row kernel, in balanced row blocks of at most 256
+  // rows (8 waves up to 128 rows, else 16). At 320 rows two 160-row blocks
+  // beat the 32-row kernel's 256 + 64 split (128 vs 153 µs on the 80-node
+  // sweep tree). Head dim 64: the 16-row kernel up to 128 rows, else the
+  // 32-row kernel.
+  p.rows16 = mfma && (d == 128 || rows <= 128);
   if (p.rows16) {
-    p.nw = rows > 128 ? 16 : 8;
-    p.row_blocks = 1;
-    p.rows_per_wg = 16 * p.nw;
+    // Row blocks of at most 256 rows, balanced, in multiples of 16.
+    p.row_blocks = (rows + 255) / 256;
+    p.rows_per_wg = ((rows + p.row_blocks - 1) / p.row_blocks + 15) / 16 * 16;
+    p.nw = p.rows_per_wg > 128 ? 16 : 8;
   } else {
     if (mfma) {
       p.nw = 8;
@@ -1295,8 +1305,7 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
       hipLaunchKernelGGL((tree_attn_m16<64, 8>), grid, dim3(512), 0, st, a);
     }
   } else if (mfma) {
-    if (d == 128) hipLaunchKernelGGL((tree_attn_mfma<128, 8, kStages>), grid, dim3(512), 0, st, a);
-    else hipLaunchKernelGGL((tree_attn_mfma<64, 8, kStages>), grid, dim3(512), 0, st, a);
+    hipLaunchKernelGGL((tree_attn_mfma<64, 8, kStages>), grid, dim3(512), 0, st, a);
   } else {
     if (dtype == CURE_BF16) {
       if (d == 128) hipLaunchKernelGGL((tree_attn_valu<uint16_t, 128>), grid, dim3(256), 0, st, a);

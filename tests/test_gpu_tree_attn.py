@@ -97,14 +97,19 @@ def test_ragged_nodes_and_contexts():
 
 @pytest.mark.parametrize("hq,hkv,d,n_ufp,depth", [(32, 8, 128, 16, 4), (8, 8, 128, 16, 15),
                                                   (4, 1, 128, 8, 4), (4, 1, 64, 8, 4),
-                                                  (32, 8, 128, 2, 4)])
+                                                  (32, 8, 128, 2, 4), (64, 8, 128, 8, 4),
+                                                  (32, 4, 128, 15, 5), (32, 8, 64, 4, 4)])
 def test_row_blocking_and_wide_trees(hq, hkv, d, n_ufp, depth):
     # Rows per kv-head = nodes x group:
-    # (32,8,128,16,4): 80 x 4 = 320 -> two row blocks of the 32-row kernel;
+    # (32,8,128,16,4): 80 x 4 = 320 -> two 160-row blocks of the 16-row kernel;
     # (8,8,128,16,15): 256 nodes (the maximum), G1 -> 16-row kernel, 16 waves;
     # (4,1,128,8,4): 48 x 4 = 192 -> 16-row kernel, 12 of 16 waves;
     # (4,1,64,8,4): 192 rows at head dim 64 -> 32-row kernel;
-    # (32,8,128,2,4): 24 x 4 = 96 -> 16-row kernel, 6 of 8 waves.
+    # (32,8,128,2,4): 24 x 4 = 96 -> 16-row kernel, 6 of 8 waves;
+    # (64,8,128,8,4): 48 x 8 = 384 -> two 192-row blocks;
+    # (32,4,128,15,5): 91 x 8 = 728 -> three 256-row blocks, the last with 216
+    #   rows (its 14th wave half full); hkv 4, so the blocks sit on different XCDs;
+    # (32,8,64,4,4): 32 x 4 = 128 rows at head dim 64 -> 16-row kernel.
     say("attn rows", hq, hkv, d, n_ufp, depth)
     w = make_workload("w", batch=1, hq=hq, hkv=hkv, d=d, ctx_lens=[777], chain_len=16,
                       n_ufp=n_ufp, branch_depth=depth, seed=90)
@@ -177,8 +182,8 @@ def test_long_context_full_size_sampled():
 
 
 def test_largest_sweep_tree_full_size_sampled():
-    # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, two row blocks of
-    # the 32-row kernel, in the launch configuration the budget sweep times.
+    # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, two 160-row blocks
+    # of the 16-row kernel, in the launch configuration the budget sweep times.
     say("attn llama3_8b_ctx8k_b8_budget64 sampled")
     with Timer("generate"):
         w = preset("llama3_8b_ctx8k_b8_budget64")
