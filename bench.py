@@ -51,6 +51,7 @@ if ROOT not in sys.path:
 
 METRIC = "tree-verify step latency (µs) + KV GB/s vs HBM peak, Llama-3-8B attn shape"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # dense bf16 matrix-core peak
 DEFAULT_WORKLOAD = "llama3_8b_ctx2k_b1"
 ROTATE_BYTES = 512 << 20
 CSRC = os.path.join(ROOT, "paper_2608_00531_amd", "csrc")
@@ -297,6 +298,22 @@ def stored_traffic(call, workload):
     return int(entry["bytes_per_call"]) if h.hexdigest() == entry["sources_sha256"] else None
 
 
+def attention_flops(w):
+    """Algorithmic flops of one cure_tree_attn call: 2 * D for each of Q K^T and P V
+    over every visible (query head, key) pair. Node n of sequence b sees the ctx_len[b]
+    context rows and the depth(n) + 1 nodes of its root path, with depths taken from the
+    workload's parent array; masked pairs are not counted."""
+    total = 0
+    for b in range(w.batch):
+        depth = []
+        for n in range(int(w.n_nodes[b])):
+            p = int(w.parent[b][n])
+            depth.append(0 if p < 0 else depth[p] + 1)
+        visible = sum(int(w.ctx_len[b]) + dn + 1 for dn in depth)
+        total += 4 * w.hq * w.d * visible
+    return total
+
+
 def repair_bytes(w, step):
     """Algorithmic bytes of one cure_repair_tree call, from what it produced: the
     logits rows of the UFPs that received branches (the rows that must be
@@ -437,6 +454,8 @@ def measure(w, args, torch, pc):
              "attn": "cure_tree_attn (tree_attn_m16 or tree_attn_mfma, + attn_merge)",
              "accept": "cure_accept (accept_kernel)"}
     value = step_bytes / (ms * 1e-3) / 1e9
+    attn_flops = attention_flops(w)
+    attn_tf = attn_flops / (calls["attn"] * 1e-6) / 1e12
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -464,6 +483,12 @@ def measure(w, args, torch, pc):
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
                      "traffic": stored_traffic(dom, w.name)},
+        # The attention call against its other bound, the bf16 matrix cores (it
+        # reaches the ridge only for the widest trees).
+        "attn_mfma": {"bound": "mfma", "kernel": names["attn"],
+                      "achieved": round(attn_tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                      "unit": "TFLOP/s", "frac": round(attn_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                      "flops": attn_flops},
         "repair_tree": dict(rep_info, us=round(calls["repair"], 2),
                             roofline={"bound": "hbm", "kernel": "cure_repair_tree (topk_chunk "
                                       "+ repair_assemble)",
