@@ -95,6 +95,48 @@ def test_ragged_nodes_and_contexts():
         check_attn(w, o, lse, ref_o, ref_l)
 
 
+def _trim_trees(w, n_nodes):
+    # Keep each tree's first n_nodes[b] nodes (prefixes of a topological order
+    # are trees too) and rebuild the packed cache rows for the shorter trees.
+    w.n_nodes[:] = n_nodes
+    rows = w.ctx_len + w.n_nodes
+    off = np.concatenate([[0], np.cumsum(rows)[:-1]]).astype(np.int64)
+    k = np.concatenate([w.k[w.kv_off[b]: w.kv_off[b] + rows[b]] for b in range(w.batch)])
+    v = np.concatenate([w.v[w.kv_off[b]: w.kv_off[b] + rows[b]] for b in range(w.batch)])
+    w.kv_off, w.k, w.v, w.kv_rows = off, k, v, int(rows.sum())
+
+
+def test_row_blocks_over_ragged_trees():
+    # 80-node trees at group 4 (320 rows: two 160-row blocks) trimmed per
+    # sequence: 160 rows (the second block has nothing to do), 68 rows, an empty
+    # tree and an empty context.
+    say("attn row blocks ragged")
+    w = make_workload("rb", batch=5, ctx_lens=[500, 1200, 30, 0, 2000], chain_len=16,
+                      n_ufp=16, branch_depth=4, seed=83)
+    _trim_trees(w, [80, 40, 0, 17, 80])
+    dev = upload(w)
+    for kv_split in (0, 3):
+        o, lse, st = gpu_attn(w, dev, kv_split=kv_split)
+        torch.cuda.synchronize()
+        assert st.tolist() == [pc.CURE_OK] * w.batch
+        ref_o, ref_l = oracle_attn(w)
+        check_attn(w, o, lse, ref_o, ref_l)
+
+
+def test_largest_tree_with_gqa():
+    # 256 nodes (the maximum) at group 4: 1024 rows per kv-head, four 256-row blocks.
+    say("attn 256 nodes x group 4")
+    w = make_workload("g", batch=1, hq=16, hkv=4, ctx_lens=[333], chain_len=16, n_ufp=15,
+                      branch_depth=16, seed=84, vocab=64)
+    assert int(w.n_nodes[0]) == 256
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK]
+    ref_o, ref_l = oracle_attn(w)
+    check_attn(w, o, lse, ref_o, ref_l)
+
+
 @pytest.mark.parametrize("hq,hkv,d,n_ufp,depth", [(32, 8, 128, 16, 4), (8, 8, 128, 16, 15),
                                                   (4, 1, 128, 8, 4), (4, 1, 64, 8, 4),
                                                   (32, 8, 128, 2, 4), (64, 8, 128, 8, 4),
