@@ -987,7 +987,7 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
 // with no more registers held than that needs. The lane groups holding
 // different splits are combined with xor shuffles at the end.
 template <int D, int NB>
-__global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
+__global__ __launch_bounds__(256) void attn_merge(Args a) {
   constexpr int kLanesPerSplit = D / 4;
   constexpr int kSplitsPerLoad = kWave / kLanesPerSplit;
   constexpr int kSplitsPerBatch = kSplitsPerLoad * NB;
@@ -997,7 +997,6 @@ __global__ __launch_bounds__(256) void attn_merge(Args a, int batch) {
   const int head = blockIdx.x * 4 + wave;
   const int n = blockIdx.y;
   const int b = blockIdx.z;
-  (void)batch;
   if (head >= a.hq) return;
   const int64_t p0 = part_index(a, b, head, n, 0);
   const int sub = lane / kLanesPerSplit;            // which split of a load this lane holds
@@ -1321,13 +1320,13 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
     const int per_load = 256 / d;                       // splits per merge load
     const int nb = p.max_splits <= 2 * per_load ? 2 : p.max_splits <= 4 * per_load ? 4 : 8;
     if (d == 128) {
-      if (nb == 2) hipLaunchKernelGGL((attn_merge<128, 2>), mgrid, dim3(256), 0, st, a, batch);
-      else if (nb == 4) hipLaunchKernelGGL((attn_merge<128, 4>), mgrid, dim3(256), 0, st, a, batch);
-      else hipLaunchKernelGGL((attn_merge<128, 8>), mgrid, dim3(256), 0, st, a, batch);
+      if (nb == 2) hipLaunchKernelGGL((attn_merge<128, 2>), mgrid, dim3(256), 0, st, a);
+      else if (nb == 4) hipLaunchKernelGGL((attn_merge<128, 4>), mgrid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((attn_merge<128, 8>), mgrid, dim3(256), 0, st, a);
     } else {
-      if (nb == 2) hipLaunchKernelGGL((attn_merge<64, 2>), mgrid, dim3(256), 0, st, a, batch);
-      else if (nb == 4) hipLaunchKernelGGL((attn_merge<64, 4>), mgrid, dim3(256), 0, st, a, batch);
-      else hipLaunchKernelGGL((attn_merge<64, 8>), mgrid, dim3(256), 0, st, a, batch);
+      if (nb == 2) hipLaunchKernelGGL((attn_merge<64, 2>), mgrid, dim3(256), 0, st, a);
+      else if (nb == 4) hipLaunchKernelGGL((attn_merge<64, 4>), mgrid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((attn_merge<64, 8>), mgrid, dim3(256), 0, st, a);
     }
   }
   return launch_status();
