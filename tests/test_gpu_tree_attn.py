@@ -252,3 +252,35 @@ def test_nonpositive_scale_takes_the_general_path():
     torch.cuda.synchronize()
     ref_o, ref_l = oracle_attn(w)
     check_attn(w, o, lse, ref_o, ref_l)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_shapes(seed):
+    # Seeded random shapes: batch, GQA ratio, head dim, chain and branch shapes,
+    # ragged contexts (zero included), trees trimmed per sequence and forced
+    # split counts, so row blocks, splits and tail tiles combine freely.
+    rng = np.random.default_rng(1000 + seed)
+    batch = int(rng.integers(1, 5))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    group = int(rng.choice([1, 2, 4, 8]))
+    d = int(rng.choice([64, 128]))
+    chain = int(rng.integers(1, 17))
+    n_ufp = int(rng.integers(0, chain + 1))
+    depth = int(rng.integers(1, 17))
+    while chain + n_ufp * depth > 256:
+        n_ufp -= 1
+    ctx = [int(c) for c in rng.integers(0, 3000, size=batch)]
+    kv_split = int(rng.choice([0, 0, 1, 2, 5]))
+    say("attn random", seed, batch, hkv, group, d, chain, n_ufp, depth, ctx, kv_split)
+    w = make_workload("rand", batch=batch, hq=hkv * group, hkv=hkv, d=d, ctx_lens=ctx,
+                      chain_len=chain, n_ufp=n_ufp, branch_depth=depth, seed=2000 + seed,
+                      vocab=64)
+    n_tree = int(w.n_nodes[0])
+    _trim_trees(w, [int(rng.integers(0, n_tree + 1)) if rng.random() < 0.5 else n_tree
+                    for _ in range(batch)])
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev, kv_split=kv_split)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK] * w.batch
+    ref_o, ref_l = oracle_attn(w)
+    check_attn(w, o, lse, ref_o, ref_l)
