@@ -27,7 +27,8 @@ def run_step(w, dev):
 
 
 @pytest.mark.parametrize("name", ["tiny_fp32", "llama3_8b_ctx2k_b1",
-                                  "llama3_8b_ctx8k_b8_budget32"])
+                                  "llama3_8b_ctx8k_b8_budget32", "llama3_8b_ragged_b16",
+                                  "llama3_8b_ctx8k_b8_budget64"])
 def test_step_chain_matches_oracle_chain(name):
     say("step", name)
     w = preset(name)
