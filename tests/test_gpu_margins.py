@@ -169,3 +169,43 @@ def test_workspace_reuse_across_shapes():
             ref = oracle.margins(x[b], "bf16")
             want = oracle.ufp_select(ref["margin_f32"], 1.0, rows, 1)
             assert got["ufp_pos"][b, : int(got["ufp_cnt"][b])].tolist() == want
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_shapes_strides_and_gate(seed):
+    # Seeded random batches: row count, vocabulary (2 .. 300000, log-uniform),
+    # dtype, a row stride past the vocabulary (odd strides take the scalar
+    # path), ties at the top, rows with many -inf entries, and the UFP gate
+    # with random tau, budget and branch depth.
+    rng = np.random.default_rng(5000 + seed)
+    batch = int(rng.integers(1, 5))
+    rows = int(rng.integers(1, 40))
+    vocab = int(np.exp(rng.uniform(np.log(2), np.log(300000))))
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    pad = int(rng.choice([0, 0, 1, 3, 8]))
+    say("margins random", seed, batch, rows, vocab, dtype, pad)
+    x = (rng.standard_normal((batch, rows, vocab + pad)) * rng.uniform(0.5, 6)).astype(np.float32)
+    for b in range(batch):
+        for r in range(rows):
+            u = rng.random()
+            if u < 0.2:
+                j = rng.integers(0, vocab, size=int(rng.integers(2, 5)))
+                x[b, r, j] = x[b, r, :vocab].max() + 1.0
+            elif u < 0.3:
+                x[b, r, rng.integers(0, vocab, size=max(1, vocab // 3))] = -np.inf
+    x = _rows(x, dtype)
+    chain = int(rng.integers(1, rows + 1))
+    tau = float(rng.choice([np.inf, 1.0, 0.3, 2.5]))
+    depth = int(rng.integers(1, 6))
+    budget = int(rng.integers(0, 4 * chain + 1))
+    t = to_dev(x, dtype)[:, :, :vocab]
+    got = pc.cure_margins(t, chain_len=chain, tau=tau, repair_budget=budget, branch_depth=depth)
+    torch.cuda.synchronize()
+    _compare(np.ascontiguousarray(x[:, :, :vocab]), dtype,
+             {k: v for k, v in got.items() if k not in ("ufp_pos", "ufp_cnt")})
+    for b in range(batch):
+        ref = oracle.margins(x[b, :, :vocab], dtype)
+        want = oracle.ufp_select(ref["margin_f32"][:chain], tau, budget, depth)
+        cnt = int(got["ufp_cnt"][b])
+        assert got["ufp_pos"][b, :cnt].tolist() == want
+        assert all(p == -1 for p in got["ufp_pos"][b, cnt:].tolist())
