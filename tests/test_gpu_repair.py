@@ -204,3 +204,33 @@ def test_largest_block_and_vocabulary():
     say("repair limits: vocab 524288")
     blk = make_draft_block(batch=2, chain_len=4, vocab=524288, seed=42, n_low=2)
     run_case(blk, tau=1.0, budget=8, depth=4, scale=1.0, b_min=1, b_max=5)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_parameters(seed):
+    # Seeded random blocks and parameters: batch, chain length, vocabulary
+    # (8 .. 200000), dtype, b_min/b_max, branch depth, budget, margin scale, tau,
+    # the number of low-margin rows, -inf-heavy rows, with and without suffixes.
+    rng = np.random.default_rng(7000 + seed)
+    batch = int(rng.integers(1, 6))
+    chain = int(rng.integers(1, 17))
+    vocab = int(np.exp(rng.uniform(np.log(8), np.log(200000))))
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    b_max = int(rng.integers(1, 8))
+    b_min = int(rng.integers(0, b_max + 1))
+    depth = int(rng.integers(1, 9))
+    budget = int(rng.integers(0, chain * depth * 2 + 1))
+    while chain + budget > 256:
+        budget -= 1
+    scale = float(rng.choice([1.0, 0.5, 2.0, 0.3]))
+    tau = float(rng.choice([np.inf, 1.0, 1.5, 0.2]))
+    n_low = int(rng.integers(0, chain + 1))
+    runners = min(int(rng.integers(1, 8)), vocab - 1)
+    blk = make_draft_block(batch=batch, chain_len=chain, vocab=vocab, dtype=dtype,
+                           seed=9000 + seed, n_low=n_low, runners=runners, b_max=b_max,
+                           depth=depth, p_ninf=float(rng.choice([0.0, 0.0, 0.3])))
+    suffix = bool(rng.random() < 0.7)
+    say("repair random", seed, batch, chain, vocab, dtype, b_min, b_max, depth, budget, scale,
+        tau, suffix)
+    run_case(blk, tau=tau, budget=budget, depth=depth, scale=scale, b_min=b_min, b_max=b_max,
+             with_suffix=suffix)
