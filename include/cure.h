@@ -16,6 +16,8 @@
  *   cure_commit     the winning path committed: its cache rows moved after the
  *                   context in every layer, the emitted tokens, the new context
  *                   length and the draft-cache replay start   (Sec. 3.5, Alg. 1)
+ *   cure_read_ceiling  not a step of the method: a plain streaming read, the
+ *                   practical HBM read rate the other calls are compared with
  *
  * Conventions shared by every entry point
  *  - All array arguments are DEVICE pointers (memory the caller allocated with
