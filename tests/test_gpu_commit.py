@@ -323,3 +323,45 @@ def test_full_size_llama3_8b_32_layers():
         assert np.array_equal(_host(k[l]), exp)
     _check_tokens(got, w.token, paths, acc, bonus, w.chain_len, w.ctx_len, w.n_max)
     assert int(got["replay_start"][0]) < a
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_shapes(seed):
+    # Seeded random commits: batch, kv heads, head dim, dtype, layers, a gap
+    # between layers, chain and branch shapes, contexts and how often the target
+    # agrees with the draft (which sets how deep the winning paths run).
+    rng = np.random.default_rng(8000 + seed)
+    batch = int(rng.integers(1, 9))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    d = int(rng.choice([8, 32, 64, 128]))
+    dtype = "bf16" if rng.random() < 0.6 else "f32"
+    layers = int(rng.integers(1, 5))
+    gap = int(rng.integers(0, 20))
+    chain = int(rng.integers(1, 17))
+    n_ufp = int(rng.integers(0, chain + 1))
+    depth = int(rng.integers(1, 9))
+    while chain + n_ufp * depth > 256:
+        n_ufp -= 1
+    ctx = [int(c) for c in rng.integers(0, 300, size=batch)]
+    say("commit random shapes", seed, batch, hkv, d, dtype, layers, gap, chain, n_ufp, depth)
+    w = make_workload("c", dtype=dtype, batch=batch, hq=hkv, hkv=hkv, d=d, vocab=16,
+                      ctx_lens=ctx, chain_len=chain, n_ufp=n_ufp, branch_depth=depth,
+                      seed=8100 + seed, p_agree=float(rng.choice([0.5, 0.8, 0.95, 1.0])))
+    acc_res = _accept_all(w)
+    acc = np.array([r["acc_len"] for r in acc_res], np.int32)
+    bonus = np.array([r["bonus"] for r in acc_res], np.int32)
+    paths = _padded_paths([r["path"] for r in acc_res], acc, w.n_max)
+    rows = w.kv_rows
+    shape = (layers, rows + gap, hkv, d)
+    if dtype == "f32":
+        ck = rng.standard_normal(shape, dtype=np.float32)
+        cv = rng.standard_normal(shape, dtype=np.float32)
+    else:
+        ck = rng.integers(0, 1 << 16, shape, dtype=np.uint16)
+        cv = rng.integers(0, 1 << 16, shape, dtype=np.uint16)
+    k, v = _dev(ck), _dev(cv)
+    got = _run(k, v, w.kv_off, w.ctx_len, w.n_nodes, paths, acc, w.token, bonus, w.chain_len)
+    assert got["status"].tolist() == [pc.CURE_OK] * w.batch
+    assert np.array_equal(_host(k), _expected_cache(ck, w.kv_off, w.ctx_len, paths, acc, rows))
+    assert np.array_equal(_host(v), _expected_cache(cv, w.kv_off, w.ctx_len, paths, acc, rows))
+    _check_tokens(got, w.token, paths, acc, bonus, w.chain_len, w.ctx_len, w.n_max)
