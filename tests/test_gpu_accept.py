@@ -69,3 +69,35 @@ def test_malformed_tree_reports_minus_one():
     assert int(got["acc_len"][0]) == -1 and int(got["resync"][0]) == -1
     assert got["path"][0].tolist() == [-1] * 4
     assert int(got["acc_len"][1]) == 4 and got["path"][1].tolist() == [0, 1, 2, 3]
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_batches(seed):
+    # Seeded random batches: up to 32 sequences, n_max 1 .. 256, alphabets of
+    # 2 .. 1000 tokens, chain lengths 1 .. 32 and trees that mostly extend a
+    # chain then attach within a random span of recent nodes.
+    rng = np.random.default_rng(9500 + seed)
+    B = int(rng.integers(1, 33))
+    n_max = int(rng.integers(1, 257))
+    alpha = int(rng.choice([2, 3, 5, 50, 1000]))
+    chain = int(rng.integers(1, 33))
+    say("accept random", seed, B, n_max, alpha, chain)
+    parent = np.full((B, n_max), -1, np.int32)
+    n_nodes = rng.integers(0, n_max + 1, B).astype(np.int32)
+    span = int(rng.integers(1, 10))
+    for b in range(B):
+        for n in range(1, int(n_nodes[b])):
+            parent[b, n] = (n - 1 if (n < chain and rng.random() < 0.8)
+                            else int(rng.integers(max(-1, n - span), n)))
+    token = rng.integers(0, alpha, (B, n_max)).astype(np.int32)
+    tgt = rng.integers(0, alpha, (B, n_max)).astype(np.int32)
+    root = rng.integers(0, alpha, B).astype(np.int32)
+    got = _run(parent, token, tgt, root, n_nodes, chain)
+    for b in range(B):
+        ref = oracle.accept(parent[b], token[b], tgt[b], int(root[b]), int(n_nodes[b]), chain)
+        assert int(got["acc_len"][b]) == ref["acc_len"], b
+        assert int(got["best"][b]) == ref["best"]
+        assert int(got["bonus"][b]) == ref["bonus"]
+        assert int(got["resync"][b]) == ref["resync"]
+        p = got["path"][b].tolist()
+        assert p[: ref["acc_len"]] == ref["path"] and all(x == -1 for x in p[ref["acc_len"]:])
