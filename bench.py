@@ -84,6 +84,11 @@ def parse():
                    help="target layers in the sweep's verification cost model")
     p.add_argument("--accept-trees", type=int, default=2048,
                    help="seeded trees per budget for the sweep's mean accepted length")
+    p.add_argument("--no-targets", action="store_true",
+                   help="skip the bandwidth-bar workloads (ragged batch, long context, "
+                        "32- and 64-node repair budgets) measured beside the headline step")
+    p.add_argument("--summary", default=None,
+                   help="with --sweep: also write the sweep as a markdown summary to this path")
     return p.parse_args()
 
 
@@ -93,6 +98,7 @@ class Step:
     def __init__(self, pc, torch, w, copy, stream, commit_cache):
         L = pc.lib()
         self.L = L
+        self.stream = stream
         dev = torch.device("cuda")
         i32 = dict(dtype=torch.int32, device=dev)
         f32 = dict(dtype=torch.float32, device=dev)
@@ -146,6 +152,8 @@ class Step:
             budget, depth, ctypes.c_float(w.tau), B_MIN, B_MAX, P(copy["suffix"]),
             self.rep_nmax, P(self.rep["parent"]), P(self.rep["token"]),
             P(self.rep["n_nodes"]), P(self.rep["branch_cnt"]), P(self.rws), self.rws.numel(), s)
+        if commit_cache is None:                 # the call is not timed here
+            return
         ck, cv = commit_cache
         self.com = {k: torch.empty(B, **i32) for k in
                     ("new_ctx_len", "emit_cnt", "replay_start", "status")}
@@ -251,32 +259,160 @@ def timed_steps(torch, graphs, k, warmup):
     return wall * 1e3 / k, start.elapsed_time(end) / k
 
 
-def per_call_times(torch, steps, k):
-    """Average GPU duration of each call, from events around every eager launch.
-    A spin kernel queued first keeps the host's launch cost off the GPU timeline."""
-    names = ("margins", "attn", "accept", "repair", "commit")
+class _Dim3(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_uint32), ("y", ctypes.c_uint32), ("z", ctypes.c_uint32)]
+
+
+class _KernelNodeParams(ctypes.Structure):
+    _fields_ = [("blockDim", _Dim3), ("extra", ctypes.c_void_p), ("func", ctypes.c_void_p),
+                ("gridDim", _Dim3), ("kernelParams", ctypes.c_void_p),
+                ("sharedMemBytes", ctypes.c_uint)]
+
+
+def _hip():
+    """The HIP runtime this process already uses (the copy torch loaded)."""
+    with open("/proc/self/maps") as f:
+        paths = sorted({l.split()[-1] for l in f if "libamdhip64" in l.split()[-1]})
+    h = ctypes.CDLL(paths[0])
+    vp = ctypes.c_void_p
+    h.hipGraphGetNodes.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_size_t)]
+    h.hipGraphNodeGetType.argtypes = [vp, ctypes.POINTER(ctypes.c_int)]
+    h.hipGraphKernelNodeGetParams.argtypes = [vp, ctypes.POINTER(_KernelNodeParams)]
+    h.hipExtLaunchKernel.argtypes = [vp, _Dim3, _Dim3, vp, ctypes.c_size_t, vp, vp, vp,
+                                     ctypes.c_int]
+    h.hipEventCreate.argtypes = [ctypes.POINTER(vp)]
+    h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+    h.hipKernelNameRefByPtr.argtypes = [vp, vp]
+    h.hipKernelNameRefByPtr.restype = ctypes.c_char_p
+    return h
+
+
+def _check_hip(err, what):
+    if err != 0:
+        raise RuntimeError("%s failed with hipError %d" % (what, err))
+
+
+class KernelReplay:
+    """The kernels one library call launches, read back from a HIP graph of
+    the call (function, grid, block, arguments), so that each can be launched
+    on its own between a start and a stop HIP event (hipExtLaunchKernel): the
+    per-kernel durations behind the roofline, measured on the launch stream.
+    The captured graph is kept alive: it owns the argument copies."""
+
+    def __init__(self, torch, call, stream):
+        self.h = _hip()
+        self.stream = stream
+        self.graph = torch.cuda.CUDAGraph(keep_graph=True)
+        with torch.cuda.graph(self.graph, stream=torch.cuda.ExternalStream(stream)):
+            call()
+        raw = ctypes.c_void_p(self.graph.raw_cuda_graph())
+        n = ctypes.c_size_t(0)
+        _check_hip(self.h.hipGraphGetNodes(raw, None, ctypes.byref(n)), "hipGraphGetNodes")
+        nodes = (ctypes.c_void_p * n.value)()
+        _check_hip(self.h.hipGraphGetNodes(raw, nodes, ctypes.byref(n)), "hipGraphGetNodes")
+        self.kernels = []
+        for i in range(n.value):
+            t = ctypes.c_int(-1)
+            _check_hip(self.h.hipGraphNodeGetType(nodes[i], ctypes.byref(t)), "hipGraphNodeGetType")
+            if t.value != 0:                        # hipGraphNodeTypeKernel
+                continue
+            prm = _KernelNodeParams()
+            _check_hip(self.h.hipGraphKernelNodeGetParams(nodes[i], ctypes.byref(prm)),
+                       "hipGraphKernelNodeGetParams")
+            name = self.h.hipKernelNameRefByPtr(prm.func, ctypes.c_void_p(stream))
+            self.kernels.append((name.decode() if name else "kernel%d" % i, prm))
+
+    def names(self):
+        return [k[0] for k in self.kernels]
+
+    def launch(self, idx, ev0, ev1):
+        _, prm = self.kernels[idx]
+        _check_hip(self.h.hipExtLaunchKernel(prm.func, prm.gridDim, prm.blockDim,
+                                             prm.kernelParams, prm.sharedMemBytes,
+                                             ctypes.c_void_p(self.stream), ev0, ev1, 0),
+                   "hipExtLaunchKernel")
+
+
+def _short_kernel_name(name):
+    """A kernel's symbol as its readable name without namespace and arguments:
+    '_ZN4cure12_GLOBAL__N_113tree_attn_m16ILi128ELi8EEEvNS0_4ArgsE' ->
+    'tree_attn_m16<128, 8>' (demangled with c++filt when it is there)."""
+    import subprocess
+    try:
+        out = subprocess.run(["c++filt", name], capture_output=True, text=True,
+                             timeout=10).stdout.strip()
+    except (OSError, subprocess.SubprocessError):
+        return name
+    if not out or out == name:
+        return name
+    for pre in ("cure::(anonymous namespace)::", "cure::", "void "):
+        out = out.replace(pre, "")
+    return out.split("(")[0].strip()
+
+
+def _stats(samples):
+    a = np.asarray(samples, np.float64)
+    return {"mean": round(float(a.mean()), 2), "p10": round(float(np.percentile(a, 10)), 2),
+            "p50": round(float(np.percentile(a, 50)), 2),
+            "p90": round(float(np.percentile(a, 90)), 2), "n": int(a.size)}
+
+
+def kernel_times(torch, steps, call, k):
+    """Event-timed duration samples (µs) of every kernel that `call` launches,
+    each launched on its own K times, rotating over the input copies. Returns
+    {kernel name: samples}, in launch order."""
+    reps = [KernelReplay(torch, getattr(st, call), st.stream) for st in steps]
+    h = reps[0].h
+    names = reps[0].names()
+    out = {}
+    for ki, name in enumerate(names):
+        evs = []
+        for _ in range(k):
+            pair = (ctypes.c_void_p(), ctypes.c_void_p())
+            _check_hip(h.hipEventCreate(ctypes.byref(pair[0])), "hipEventCreate")
+            _check_hip(h.hipEventCreate(ctypes.byref(pair[1])), "hipEventCreate")
+            evs.append(pair)
+        torch.cuda.synchronize()
+        spin(torch, 5000)
+        for i in range(k):
+            reps[i % len(reps)].launch(ki, evs[i][0], evs[i][1])
+        torch.cuda.synchronize()
+        samples = []
+        for e0, e1 in evs:
+            ms = ctypes.c_float(0)
+            _check_hip(h.hipEventElapsedTime(ctypes.byref(ms), e0, e1), "hipEventElapsedTime")
+            samples.append(ms.value * 1e3)
+            h.hipEventDestroy(e0)
+            h.hipEventDestroy(e1)
+        out[_short_kernel_name(name)] = samples
+    del reps
+    return out
+
+
+CALLS = ("margins", "attn", "accept", "repair", "commit")
+
+
+def per_call_samples(torch, steps, k, calls=CALLS, warmup=0):
+    """GPU duration samples (µs) of each call, from HIP events around every
+    eager launch on the launch stream, k rounds rotating over the input copies.
+    A spin kernel queued first keeps the host's launch cost off the GPU
+    timeline."""
     n = len(steps)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(k)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(k)]
+    for i in range(warmup):
+        for name in calls:
+            getattr(steps[i % n], name)()
     torch.cuda.synchronize()
     spin(torch, 25000)
     for i in range(k):
         s = steps[i % n]
         ev[i][0].record()
-        s.margins()
-        ev[i][1].record()
-        s.attn()
-        ev[i][2].record()
-        s.accept()
-        ev[i][3].record()
-        s.repair()
-        ev[i][4].record()
-        s.commit()
-        ev[i][5].record()
+        for j, name in enumerate(calls):
+            getattr(s, name)()
+            ev[i][j + 1].record()
     torch.cuda.synchronize()
-    out = {}
-    for j, name in enumerate(names):
-        out[name] = float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(k)])) * 1e3
-    return out
+    return {name: [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(k)]
+            for j, name in enumerate(calls)}
 
 
 def stored_traffic(call, workload):
@@ -372,14 +508,9 @@ def commit_bytes(w, step, layers):
     return total, {"layers": layers, "rows_moved": moved, "bytes": total}
 
 
-def cpu_baseline(w, algo_bytes, budget_s):
+def _oracle_steps(w, budget_s):
+    """Whole oracle steps of workload w for about budget_s seconds: (steps, s/step)."""
     import oracle
-    try:
-        import threadpoolctl
-        info = threadpoolctl.threadpool_info()
-        threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
-    except Exception:
-        threads = 1
     t0 = time.perf_counter()
     reps = 0
     while True:
@@ -394,12 +525,30 @@ def cpu_baseline(w, algo_bytes, budget_s):
         reps += 1
         if time.perf_counter() - t0 >= budget_s:
             break
-    dt = (time.perf_counter() - t0) / reps
+    return reps, (time.perf_counter() - t0) / reps
+
+
+def cpu_baseline(w, algo_bytes, budget_s):
+    """The CPU oracle on this host over the same workload: about budget_s seconds
+    with the BLAS thread pool at its default size (the threads the oracle's
+    matrix-vector products use; its sorts and walks run on one thread), then
+    about budget_s / 2 seconds with one thread in all."""
+    import threadpoolctl
+    host_cores = len(os.sched_getaffinity(0))
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    reps, dt = _oracle_steps(w, budget_s)
+    with threadpoolctl.threadpool_limits(limits=1):
+        reps1, dt1 = _oracle_steps(w, budget_s / 2)
     return {"value": round(algo_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(threads),
-            "kind": "oracle", "ms_per_step": round(dt * 1e3, 1),
+            "host_cores": host_cores, "kind": "oracle", "ms_per_step": round(dt * 1e3, 1),
+            "single_thread": {"value": round(algo_bytes / dt1 / 1e9, 4), "unit": "GB/s",
+                              "cores": 1, "ms_per_step": round(dt1 * 1e3, 1), "steps": reps1},
             "sample": "%d full oracle step(s) of workload %s (margins+UFP and accept per "
-                      "sequence, float64 tree attention for every node and head); BLAS "
-                      "threads=%d, sorts single-threaded" % (reps, w.name, threads)}
+                      "sequence, float64 tree attention for every node and head) with %d "
+                      "BLAS threads (sorts and walks on one thread), then %d step(s) on one "
+                      "thread; host has %d cores available" % (reps, w.name, threads, reps1,
+                                                               host_cores)}
 
 
 def measure(w, args, torch, pc):
@@ -432,7 +581,10 @@ def measure(w, args, torch, pc):
         for st, (t1, al, o) in zip(steps, ref):
             assert torch.equal(st.m["top1_idx"], t1) and torch.equal(st.acc["acc_len"], al)
             assert torch.equal(st.o, o)
-        calls = per_call_times(torch, steps, min(args.steps, 100))
+        k_calls = min(args.steps, 100)
+        call_samples = per_call_samples(torch, steps, k_calls)
+        kern = {c: kernel_times(torch, steps, c, k_calls) for c in ("margins", "attn", "accept")}
+    calls = {c: float(np.mean(v)) for c, v in call_samples.items()}
     status = steps[0].status.cpu().tolist()
     assert status == [0] * w.batch, status
     acc_len = steps[0].acc["acc_len"].float().cpu()
@@ -445,17 +597,27 @@ def measure(w, args, torch, pc):
     kernels = {}
     for name, us in calls.items():
         gbs = call_bytes[name] / (us * 1e-6) / 1e9
-        kernels[name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
-                         "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
-    step_calls = {k: v for k, v in calls.items() if k not in ("repair", "commit")}
-    dom = max(step_calls, key=step_calls.get)
-    dom_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
-    names = {"margins": "cure_margins (margins_kernel)",
-             "attn": "cure_tree_attn (tree_attn_m16 or tree_attn_mfma, + attn_merge)",
-             "accept": "cure_accept (accept_kernel)"}
+        kernels[name] = dict(us=round(us, 2), **{k: v for k, v in _stats(call_samples[name]).items()
+                                                 if k != "mean"},
+                             **{"GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)})
+    # Kernel level: every kernel of the step's calls launched on its own between
+    # HIP events. The dominant kernel is the longest; its call's algorithmic
+    # bytes are all attributed to it (the others move only partials or results).
+    kernel_level = {}
+    for c, ks in kern.items():
+        for kname, samples in ks.items():
+            kernel_level[kname] = dict(call=c, **_stats(samples))
+    dom_k = max(kernel_level, key=lambda n: kernel_level[n]["mean"])
+    dom = kernel_level[dom_k]["call"]
+    dom_us = kernel_level[dom_k]["mean"]
+    dom_gbs = call_bytes[dom] / (dom_us * 1e-6) / 1e9
+    call_gbs = call_bytes[dom] / (calls[dom] * 1e-6) / 1e9
     value = step_bytes / (ms * 1e-3) / 1e9
     attn_flops = attention_flops(w)
-    attn_tf = attn_flops / (calls["attn"] * 1e-6) / 1e12
+    attn_k = max((n for n in kernel_level if kernel_level[n]["call"] == "attn"),
+                 key=lambda n: kernel_level[n]["mean"])
+    attn_tf = attn_flops / (kernel_level[attn_k]["mean"] * 1e-6) / 1e12
+    attn_tf_call = attn_flops / (calls["attn"] * 1e-6) / 1e12
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -479,15 +641,20 @@ def measure(w, args, torch, pc):
         "kernels": kernels,
         # Mean accepted draft length of the step's sequences (tokens emitted = +1).
         "acc_len_mean": round(float(acc_len.mean()), 3),
-        "roofline": {"bound": "hbm", "kernel": names[dom], "achieved": round(dom_gbs, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "kernel_level": kernel_level,
+        "roofline": {"bound": "hbm", "kernel": dom_k, "call": dom,
+                     "achieved": round(dom_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "kernel_us": dom_us, "bytes": call_bytes[dom],
+                     "call_us": round(calls[dom], 2),
+                     "call_frac": round(call_gbs / HBM_PEAK_GBS, 4),
                      "traffic": stored_traffic(dom, w.name)},
-        # The attention call against its other bound, the bf16 matrix cores (it
+        # The attention kernel against its other bound, the bf16 matrix cores (it
         # reaches the ridge only for the widest trees).
-        "attn_mfma": {"bound": "mfma", "kernel": names["attn"],
+        "attn_mfma": {"bound": "mfma", "kernel": attn_k,
                       "achieved": round(attn_tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                       "unit": "TFLOP/s", "frac": round(attn_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                      "call_frac": round(attn_tf_call / MFMA_BF16_PEAK_TFLOPS, 4),
                       "flops": attn_flops},
         "repair_tree": dict(rep_info, us=round(calls["repair"], 2),
                             roofline={"bound": "hbm", "kernel": "cure_repair_tree (topk_chunk "
@@ -507,6 +674,74 @@ def measure(w, args, torch, pc):
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, step_bytes, args.cpu_seconds)
     return line
+
+# The bandwidth bars: the verification attention at 70 % and the margin pass at
+# 80 % of the HBM peak, on the workloads where each is judged.
+TARGETS = (
+    ("llama3_8b_ragged_b16", (("margins", 0.80), ("attn", 0.70))),
+    ("llama3_8b_ctx32k_b4", (("attn", 0.70),)),
+    ("llama3_8b_ctx8k_b8_budget32", (("attn", 0.70),)),
+    ("llama3_8b_ctx8k_b8_budget64", (("attn", 0.70),)),
+)
+
+
+def measure_targets(args, torch, pc):
+    """For each bar: the call's duration (HIP events around each eager call)
+    and the duration of each of its kernels launched on its own (HIP events on
+    the launch stream), with mean, p10, median and p90 over 200 launches after
+    20 warm-up calls, rotating over >= 512 MB of input copies; the fraction of
+    the HBM peak at call and at kernel level (algorithmic bytes over the mean,
+    and over the median); the stored per-call HBM traffic."""
+    from synth import algorithmic_bytes, preset
+    k = 200
+    out = {}
+    for wname, checks in TARGETS:
+        w = preset(wname)
+        ab = algorithmic_bytes(w)
+        base = upload_copy(torch, w)
+        per_copy = sum(base[c].numel() * base[c].element_size() for c in ("logits", "q", "k", "v"))
+        ncopy = max(3, math.ceil(ROTATE_BYTES / per_copy))
+        copies = [base] + [replicate(torch, base) for _ in range(ncopy - 1)]
+        stream = torch.cuda.Stream()
+        names = tuple(c for c, _ in checks)
+        with torch.cuda.stream(stream):
+            steps = [Step(pc, torch, w, c, stream.cuda_stream, None) for c in copies]
+            for st in steps:
+                st.run()
+            torch.cuda.synchronize()
+            assert steps[0].status.cpu().tolist() == [0] * w.batch
+            samples = per_call_samples(torch, steps, k, calls=names, warmup=20)
+            kern = {c: kernel_times(torch, steps, c, k) for c in names}
+        flops = attention_flops(w)
+        for c, bar in checks:
+            nbytes = ab["margins"] if c == "margins" else ab["attention"]
+            cs = _stats(samples[c])
+            ks = {n: _stats(v) for n, v in kern[c].items()}
+            dom = max(ks, key=lambda n: ks[n]["mean"])
+            frac = lambda us: round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+            traffic = stored_traffic(c, wname)
+            entry = {"workload": wname, "call": c, "bar": bar, "bytes": nbytes,
+                     "call_us": cs, "kernels": ks, "dominant_kernel": dom,
+                     "frac": {"call": frac(cs["mean"]), "kernel": frac(ks[dom]["mean"]),
+                              "call_p50": frac(cs["p50"]), "kernel_p50": frac(ks[dom]["p50"])},
+                     "bar_call_us": round(nbytes / (bar * HBM_PEAK_GBS * 1e9) * 1e6, 2),
+                     "traffic": traffic,
+                     "traffic_ratio": round(traffic / nbytes, 4) if traffic else None}
+            if c == "attn":
+                tf = lambda us: round(flops / (us * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+                entry["flops"] = flops
+                entry["mfma_frac"] = {"call": tf(cs["mean"]), "kernel": tf(ks[dom]["mean"])}
+            out["%s@%s" % (c, wname)] = entry
+            print("[targets] %s %s: call %.2f us (p50 %.2f), %s %.2f us, frac call %.3f "
+                  "kernel %.3f (bar %.2f)" % (wname, c, cs["mean"], cs["p50"], dom,
+                                              ks[dom]["mean"], entry["frac"]["call"],
+                                              entry["frac"]["kernel"], bar),
+                  file=sys.stderr, flush=True)
+        del steps, copies, base, w
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
+
 
 SWEEP_BUDGETS = (0, 8, 16, 32, 64)
 # Parameters of a Llama-3-8B-class target for the sweep's cost model: its
@@ -532,6 +767,113 @@ def mean_accepted(pc, torch, budget, n_trees, seed):
     return float(acc.mean()), float(acc.std() / math.sqrt(len(acc))), float(out["resync"].float().mean())
 
 
+def tpot_model(c_d_us, c_v_us, mean_accepted):
+    """Sec. 3.1's cost model per sequence: one decoding step costs the draft
+    overhead C_d plus the verification cost C_v and emits the E[a] accepted
+    draft tokens plus the bonus token, so the time per output token is
+    (C_d + C_v) / (E[a] + 1) (microseconds)."""
+    return (c_d_us + c_v_us) / (mean_accepted + 1.0)
+
+
+def rate_model(mean_accepted, batch, c_d_us, c_v_us):
+    """Sec. 3.1's generation rate, (E[a] + 1) / (C_d + C_v) per sequence, for a
+    batch of sequences verified together: output tokens per second."""
+    return batch / (tpot_model(c_d_us, c_v_us, mean_accepted) * 1e-6)
+
+
+def speedup(tpot_ref, tpot):
+    """Speedup as Table 1 reports it (Sec. 4.1's metric): the ratio of the
+    reference's time per output token to the method's."""
+    return tpot_ref / tpot
+
+
+def accept_gain(accepted_ref, accepted):
+    """Relative gain in accepted tokens per step over a reference (Sec. 4.2
+    quotes the gain over the single-path parallel draft this way)."""
+    return accepted / accepted_ref - 1.0
+
+
+def verify_cost(layers, attn_us, margins_us, accept_us, weights_us):
+    """C_v(N) of the sweep: every target layer's verification attention over the
+    tree, the margin pass over the node logits, the acceptance walk, and one
+    streaming read of the target's weights."""
+    return layers * attn_us + margins_us + accept_us + weights_us
+
+
+def rate_table(rows, t_weights_us, layers, batch, ratios=(0.25, 0.5, 1.0, 2.0)):
+    """The sweep's rate model over measured rows.
+
+    rows: dicts with budget, tree_nodes, mean_accepted and the measured attn_us,
+    margins_us, accept_us of that budget's step. For each draft cost C_d =
+    ratio x t_weights it adds the modelled tokens/s of every row and picks the
+    budget with the highest rate (its gain over budget 0 is the speedup of its
+    time per output token over budget 0's). Returns (table, best)."""
+    table = []
+    for row in rows:
+        cv = verify_cost(layers, row["attn_us"], row["margins_us"], row["accept_us"], t_weights_us)
+        table.append({"budget": row["budget"], "tree_nodes": row["tree_nodes"],
+                      "mean_accepted": row["mean_accepted"], "attn_us": row["attn_us"],
+                      "c_v_us": round(cv, 1), "_cv": cv})
+    best = {}
+    for ratio in ratios:
+        cd = ratio * t_weights_us
+        scored = []
+        for row in table:
+            rate = rate_model(row["mean_accepted"], batch, cd, row["_cv"])
+            row["tokens_per_s_cd%.2g" % ratio] = round(rate, 1)
+            scored.append((rate, -row["budget"], row))
+        top = max(scored, key=lambda s: (s[0], s[1]))[2]
+        base = table[0]
+        gain = speedup(tpot_model(cd, base["_cv"], base["mean_accepted"]),
+                       tpot_model(cd, top["_cv"], top["mean_accepted"]))
+        best["cd_%.2g_x_weights" % ratio] = {
+            "budget": top["budget"],
+            "tokens_per_s": round(rate_model(top["mean_accepted"], batch, cd, top["_cv"]), 1),
+            "gain_vs_budget0": round(gain, 4)}
+    for row in table:
+        del row["_cv"]
+    return table, best
+
+
+def write_sweep_summary(args, rows, summary):
+    """The sweep as a short markdown summary: per budget the tree size, the
+    measured call times, E[a] with its standard error, and the modelled rate per
+    draft cost, then the best budget per draft cost."""
+    cmd = "python3 bench.py --sweep --steps %d --warmup %d --cpu-seconds %g --accept-trees %d " \
+          "--layers %d --summary %s" % (args.steps, args.warmup, args.cpu_seconds,
+                                        args.accept_trees, args.layers, args.summary)
+    out = ["# Acceptance-compute sweep: batch 8, context 8192, chain 16, depth-4 branches", "",
+           "Command (from the repository root):", "", "    " + cmd, "",
+           "Measured on this GPU: the per-call times (HIP events, mean of the eager "
+           "calls) and E[a] (cure_accept over %d seeded trees per budget against the "
+           "synthetic target that agrees with each node with probability 0.8). Modelled: "
+           "C_v = %d x attention + margins + accept + one read of the target's weights "
+           "(%.1f µs at the margin pass's %.1f GB/s), and C_d in multiples of that "
+           "read. Rate = (E[a] + 1) x %d / (C_d + C_v)."
+           % (args.accept_trees, summary["layers"], summary["t_weights_us"],
+              summary["weights_gbps"], summary["batch"]), ""]
+    ratios = [k for k in summary["rows"][0] if k.startswith("tokens_per_s_cd")]
+    head = ["budget", "nodes", "attention µs", "attention frac of 8 TB/s", "margins µs",
+            "accept µs", "step µs", "E[a] ± se", "C_v µs"] + \
+           ["tok/s, C_d = %s x weights" % k[len("tokens_per_s_cd"):] for k in ratios]
+    out.append("| " + " | ".join(head) + " |")
+    out.append("|" + "---|" * len(head))
+    for r, t in zip(rows, summary["rows"]):
+        cells = [r["budget"], r["tree_nodes"], r["attn_us"], r["attn_frac_hbm"], r["margins_us"],
+                 r["accept_us"], r["step_us"], "%.3f ± %.3f" % (r["mean_accepted"],
+                                                             r["mean_accepted_se"]),
+                 t["c_v_us"]] + [t[k] for k in ratios]
+        out.append("| " + " | ".join(str(c) for c in cells) + " |")
+    out += ["", "Best budget per draft cost:", ""]
+    for k, v in summary["best_budget"].items():
+        out.append("* C_d = %s x weights: budget %d, %.1f tok/s, %.4f x budget 0's rate"
+                   % (k[len("cd_"):-len("_x_weights")], v["budget"], v["tokens_per_s"],
+                      v["gain_vs_budget0"]))
+    os.makedirs(os.path.dirname(os.path.abspath(args.summary)), exist_ok=True)
+    with open(args.summary, "w") as f:
+        f.write("\n".join(out) + "\n")
+
+
 def sweep(args, torch, pc):
     """Acceptance-compute trade-off (Sec. 3.1's rate model): for each repair
     budget, the measured verify step and the mean accepted length, then the
@@ -544,44 +886,40 @@ def sweep(args, torch, pc):
     pass bandwidth (one streaming read of the weights per verification pass),
     and a synthetic draft cost C_d given as multiples of t_weights (the paper's
     drafter is a target-sized block-parallel model: one forward, C_d ~ t_weights).
-    The budget that maximises the rate is reported per C_d."""
+    The budget that maximises the rate is reported per C_d; with --summary the
+    per-budget figures and that choice are also written as a markdown table."""
     from synth import preset
     rows = []
+    batch = None
     for budget in SWEEP_BUDGETS:
         w = preset("llama3_8b_ctx8k_b8_budget%d" % budget)
+        batch = w.batch
         line = measure(w, args, torch, pc)
         ea, ea_se, resync = mean_accepted(pc, torch, budget, args.accept_trees, budget)
         line["sweep"] = {"budget": budget, "tree_nodes": int(w.n_nodes.max()),
                          "mean_accepted": round(ea, 4), "mean_accepted_se": round(ea_se, 4),
                          "resync_rate": round(resync, 4), "accept_trees": args.accept_trees}
         print(json.dumps(line), flush=True)
-        rows.append((budget, w, line, ea))
-    # Weight streaming at the bandwidth the margin pass reached on this GPU.
-    bw = max(r[2]["kernels"]["margins"]["GB/s"] for r in rows) * 1e9
-    t_weights = TARGET_PARAMS * TARGET_BYTES_PER_PARAM / bw * 1e6
-    table = []
-    for budget, w, line, ea in rows:
         k = line["kernels"]
-        cv = args.layers * k["attn"]["us"] + k["margins"]["us"] + k["accept"]["us"] + t_weights
-        table.append({"budget": budget, "tree_nodes": int(w.n_nodes.max()),
-                      "mean_accepted": round(ea, 4), "attn_us": k["attn"]["us"],
-                      "c_v_us": round(cv, 1)})
-    best = {}
-    for ratio in (0.25, 0.5, 1.0, 2.0):
-        cd = ratio * t_weights
-        rates = []
-        for row in table:
-            rate = (row["mean_accepted"] + 1) * 8 / ((cd + row["c_v_us"]) * 1e-6)
-            row["tokens_per_s_cd%.2g" % ratio] = round(rate, 1)
-            rates.append((rate, row["budget"]))
-        top = max(rates)
-        best["cd_%.2g_x_weights" % ratio] = {"budget": top[1], "tokens_per_s": round(top[0], 1),
-                                             "gain_vs_budget0": round(top[0] / rates[0][0], 4)}
-    print(json.dumps({"sweep_summary": {
+        rows.append({"budget": budget, "tree_nodes": int(w.n_nodes.max()),
+                     "mean_accepted": round(ea, 4), "mean_accepted_se": round(ea_se, 4),
+                     "attn_us": k["attn"]["us"], "margins_us": k["margins"]["us"],
+                     "accept_us": k["accept"]["us"], "step_us": line["step_latency_us"],
+                     "margins_gbps": k["margins"]["GB/s"],
+                     "attn_frac_hbm": k["attn"]["frac_hbm"]})
+        del w
+    # Weight streaming at the bandwidth the margin pass reached on this GPU.
+    bw = max(r["margins_gbps"] for r in rows) * 1e9
+    t_weights = TARGET_PARAMS * TARGET_BYTES_PER_PARAM / bw * 1e6
+    table, best = rate_table(rows, t_weights, args.layers, batch)
+    summary = {
         "model": "rate = (E[a] + 1) * batch / (C_d + C_v(N)); C_v = layers * attn + margins + "
                  "accept + weight streaming; C_d synthetic, in multiples of the weight stream",
-        "layers": args.layers, "batch": 8, "t_weights_us": round(t_weights, 1),
-        "weights_gbps": round(bw / 1e9, 1), "rows": table, "best_budget": best}}), flush=True)
+        "layers": args.layers, "batch": batch, "t_weights_us": round(t_weights, 1),
+        "weights_gbps": round(bw / 1e9, 1), "rows": table, "best_budget": best}
+    print(json.dumps({"sweep_summary": summary}), flush=True)
+    if args.summary:
+        write_sweep_summary(args, rows, summary)
 
 
 def main():
@@ -599,7 +937,10 @@ def main():
     if args.sweep:
         sweep(args, torch, pc)
         return
-    print(json.dumps(measure(preset(args.workload), args, torch, pc)), flush=True)
+    line = measure(preset(args.workload), args, torch, pc)
+    if not args.no_targets:
+        line["targets"] = measure_targets(args, torch, pc)
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":
