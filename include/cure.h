@@ -16,6 +16,8 @@
  *   cure_commit     the winning path committed: its cache rows moved after the
  *                   context in every layer, the emitted tokens, the new context
  *                   length and the draft-cache replay start   (Sec. 3.5, Alg. 1)
+ *   cure_margins_noalloc  cure_margins for callers that cannot allocate: its
+ *                   scratch is a fixed array inside the library
  *   cure_read_ceiling  not a step of the method: a plain streaming read, the
  *                   practical HBM read rate the other calls are compared with
  *
@@ -23,7 +25,9 @@
  *  - All array arguments are DEVICE pointers (memory the caller allocated with
  *    hipMalloc or equivalent), except those whose name starts with host_.
  *    The library allocates no device memory and keeps no state beyond a cached
- *    device-property query; the caller owns every buffer.
+ *    device-property query (and the static scratch array of
+ *    cure_margins_noalloc, part of its code object); the caller owns every
+ *    buffer.
  *  - stream is a hipStream_t passed as void* (NULL = the legacy default stream).
  *    Calls only enqueue work: they return before the work runs, and the outputs
  *    are valid once the stream reaches that point.
@@ -106,6 +110,31 @@ cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch, int32
                          int32_t chain_len, float tau, int32_t repair_budget,
                          int32_t branch_depth, int32_t* ufp_pos, int32_t* ufp_cnt,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Allocation-free margin pass, for callers that cannot allocate device memory
+ * (code under HIP stream capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same pass, outputs and UFP gate as cure_margins, with no
+ * workspace argument. Its scratch (the chunk results of rows split across
+ * workgroups, 32 bytes per row and chunk) lives in a fixed device array of
+ * cure_margins_noalloc_scratch_bytes() bytes (256 KiB) inside the library,
+ * one per GPU the library runs on, held until the process ends. The call
+ * itself allocates nothing; its first use on a device looks up that device's
+ * copy of the array (hipGetSymbolAddress).
+ * Returns CURE_ERR_UNSUPPORTED when the call would need more scratch than the
+ * array holds (never on a 256-CU MI355X, whose plans need at most 32 KiB),
+ * CURE_ERR_HIP when the array cannot be found on the current device, else as
+ * cure_margins. Every call on one GPU shares that GPU's array and leaves its
+ * contents behind: calls whose work may overlap on the GPU (different streams
+ * without ordering between them) race and must not be issued. */
+size_t cure_margins_noalloc_scratch_bytes(void);
+
+cure_status cure_margins_noalloc(const void* logits, int32_t dtype, int32_t batch,
+                                 int32_t rows, int32_t vocab, int64_t ld,
+                                 float* top1_val, int32_t* top1_idx, float* top2_val,
+                                 int32_t* top2_idx, float* lse, float* margin,
+                                 int32_t chain_len, float tau, int32_t repair_budget,
+                                 int32_t branch_depth, int32_t* ufp_pos, int32_t* ufp_cnt,
+                                 void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Tree-attention verification -- Sec. 3.2 (phase 3), Sec. 3.4, Sec. 3.5.

@@ -21,6 +21,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.hpp"
 #include "host_util.hpp"
@@ -383,6 +384,121 @@ __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
   }
 }
 
+// Scratch of the allocation-free entry point: the chunk results of one call
+// (32 bytes per row and chunk). The library's code object holds one copy per
+// GPU it is loaded on, for the life of the process; host code reaches it only
+// through the address hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = 256 * 1024;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct Plan {
+  int splits, chunk;
+};
+
+// Enough workgroups to cover the GPU kTargetWgsPerCu times over, with chunks
+// of about kMinChunk entries or more: at most ceil(vocab / kMinChunk) splits,
+// so a small batch's chunk fits one loop step of each register set (all its
+// loads in flight at once).
+Plan make_plan(int64_t nrow, int32_t vocab) {
+  int splits = (int)((kTargetWgsPerCu * (int64_t)device_cu_count() + nrow - 1) / nrow);
+  splits = std::max(1, std::min(splits, std::min(kMaxSplits, (vocab + kMinChunk - 1) / kMinChunk)));
+  int chunk = (vocab + splits - 1) / splits;
+  chunk = (chunk + kVec - 1) / kVec * kVec;
+  splits = (vocab + chunk - 1) / chunk;
+  return Plan{splits, chunk};
+}
+
+// Host-side argument checks shared by both entry points.
+cure_status check_args(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
+                       int32_t vocab, int64_t ld, const float* top1_val,
+                       const int32_t* top1_idx, const float* top2_val,
+                       const int32_t* top2_idx, const float* lse, const float* margin,
+                       int32_t chain_len, int32_t repair_budget, int32_t branch_depth,
+                       const int32_t* ufp_pos, const int32_t* ufp_cnt) {
+  if (dtype != CURE_F32 && dtype != CURE_BF16) return CURE_ERR_INVALID_ARG;
+  if (batch < 0 || rows < 0) return CURE_ERR_INVALID_ARG;
+  if (batch == 0 || rows == 0) return CURE_OK;
+  if (vocab < 2 || ld < vocab) return CURE_ERR_INVALID_ARG;
+  if (!logits || !top1_val || !top1_idx || !top2_val || !top2_idx || !lse || !margin)
+    return CURE_ERR_INVALID_ARG;
+  const bool gate = ufp_pos != nullptr || ufp_cnt != nullptr;
+  if (gate) {
+    if (!ufp_pos || !ufp_cnt) return CURE_ERR_INVALID_ARG;
+    if (chain_len < 1 || chain_len > rows || branch_depth < 1 || repair_budget < 0)
+      return CURE_ERR_INVALID_ARG;
+    if (chain_len > kMaxGateChain) return CURE_ERR_UNSUPPORTED;
+  }
+  if ((int64_t)batch * rows > INT32_MAX / kMaxSplits) return CURE_ERR_UNSUPPORTED;
+  return CURE_OK;
+}
+
+// Launches the pass; `partials` holds the plan's chunk results (nrow * splits
+// records) when rows are split. The arguments have passed check_args.
+cure_status launch(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
+                   int32_t vocab, int64_t ld, float* top1_val, int32_t* top1_idx,
+                   float* top2_val, int32_t* top2_idx, float* lse, float* margin,
+                   int32_t chain_len, float tau, int32_t repair_budget, int32_t branch_depth,
+                   int32_t* ufp_pos, int32_t* ufp_cnt, const Plan& pl, void* partials,
+                   void* stream) {
+  const bool gate = ufp_pos != nullptr;
+  const int64_t nrow = (int64_t)batch * rows;
+  const size_t esize = dtype == CURE_F32 ? 4 : 2;
+  const bool vec_ok = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
+                      ((size_t)ld * esize) % 16 == 0;
+
+  Args a;
+  a.logits = logits;
+  a.ld = ld;
+  a.rows = rows;
+  a.vocab = vocab;
+  a.splits = pl.splits;
+  a.chunk = pl.chunk;
+  const int per_iter = kThreads * kVec * kUnroll;
+  a.iters = (pl.chunk + per_iter - 1) / per_iter;
+  a.top1_val = top1_val;
+  a.top1_idx = top1_idx;
+  a.top2_val = top2_val;
+  a.top2_idx = top2_idx;
+  a.lse = lse;
+  a.margin = margin;
+  a.chain_len = gate ? chain_len : 0;
+  a.max_ufp = gate ? repair_budget / branch_depth : 0;
+  a.tau = tau;
+  a.ufp_pos = gate ? ufp_pos : nullptr;
+  a.ufp_cnt = gate ? ufp_cnt : nullptr;
+  a.partials = reinterpret_cast<Partial*>(partials);
+
+  const dim3 grid((unsigned)(nrow * pl.splits)), block(kThreads);
+  hipStream_t s = as_stream(stream);
+  if (dtype == CURE_BF16) {
+    if (vec_ok) hipLaunchKernelGGL((margins_kernel<uint16_t, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((margins_kernel<uint16_t, false>), grid, block, 0, s, a);
+  } else {
+    if (vec_ok) hipLaunchKernelGGL((margins_kernel<float, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((margins_kernel<float, false>), grid, block, 0, s, a);
+  }
+  if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
+  if (pl.splits > 1 || gate)
+    hipLaunchKernelGGL(margins_finish, dim3(batch), block, 0, s, a);
+  return launch_status();
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (each GPU holds its own copy of the array at its own address).
+void* scratch_address() {
+  static std::mutex mu;
+  static void* cached[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cached[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    cached[dev] = p;
+  }
+  return cached[dev];
+}
+
 }  // namespace
 }  // namespace cure
 
@@ -401,72 +517,41 @@ extern "C" cure_status cure_margins(const void* logits, int32_t dtype, int32_t b
                                     int32_t repair_budget, int32_t branch_depth,
                                     int32_t* ufp_pos, int32_t* ufp_cnt, void* workspace,
                                     size_t workspace_bytes, void* stream) {
-  if (dtype != CURE_F32 && dtype != CURE_BF16) return CURE_ERR_INVALID_ARG;
-  if (batch < 0 || rows < 0) return CURE_ERR_INVALID_ARG;
-  if (batch == 0 || rows == 0) return CURE_OK;
-  if (vocab < 2 || ld < vocab) return CURE_ERR_INVALID_ARG;
-  if (!logits || !top1_val || !top1_idx || !top2_val || !top2_idx || !lse || !margin)
-    return CURE_ERR_INVALID_ARG;
-  const bool gate = ufp_pos != nullptr || ufp_cnt != nullptr;
-  if (gate) {
-    if (!ufp_pos || !ufp_cnt) return CURE_ERR_INVALID_ARG;
-    if (chain_len < 1 || chain_len > rows || branch_depth < 1 || repair_budget < 0)
-      return CURE_ERR_INVALID_ARG;
-    if (chain_len > kMaxGateChain) return CURE_ERR_UNSUPPORTED;
-  }
-  const int64_t nrow = (int64_t)batch * rows;
-  if (nrow > INT32_MAX / kMaxSplits) return CURE_ERR_UNSUPPORTED;
-
-  // Enough workgroups to cover the GPU kTargetWgsPerCu times over, with chunks
-  // of about kMinChunk entries or more: at most ceil(vocab / kMinChunk) splits,
-  // so a small batch's chunk fits one loop step of each register set (all its
-  // loads in flight at once).
-  int splits = (int)((kTargetWgsPerCu * (int64_t)device_cu_count() + nrow - 1) / nrow);
-  splits = std::max(1, std::min(splits, std::min(kMaxSplits, (vocab + kMinChunk - 1) / kMinChunk)));
-  int chunk = (vocab + splits - 1) / splits;
-  chunk = (chunk + kVec - 1) / kVec * kVec;
-  splits = (vocab + chunk - 1) / chunk;
-  if (splits > 1 &&
+  const cure_status st = check_args(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx,
+                                    top2_val, top2_idx, lse, margin, chain_len, repair_budget,
+                                    branch_depth, ufp_pos, ufp_cnt);
+  if (st != CURE_OK || batch == 0 || rows == 0) return st;
+  const Plan pl = make_plan((int64_t)batch * rows, vocab);
+  if (pl.splits > 1 &&
       (!workspace || workspace_bytes < cure_margins_workspace_size(batch, rows, vocab)))
     return CURE_ERR_WORKSPACE;
+  return launch(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx, top2_val, top2_idx,
+                lse, margin, chain_len, tau, repair_budget, branch_depth, ufp_pos, ufp_cnt, pl,
+                workspace, stream);
+}
 
-  const size_t esize = dtype == CURE_F32 ? 4 : 2;
-  const bool vec_ok = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
-                      ((size_t)ld * esize) % 16 == 0;
+extern "C" size_t cure_margins_noalloc_scratch_bytes(void) { return kScratchBytes; }
 
-  Args a;
-  a.logits = logits;
-  a.ld = ld;
-  a.rows = rows;
-  a.vocab = vocab;
-  a.splits = splits;
-  a.chunk = chunk;
-  const int per_iter = kThreads * kVec * kUnroll;
-  a.iters = (chunk + per_iter - 1) / per_iter;
-  a.top1_val = top1_val;
-  a.top1_idx = top1_idx;
-  a.top2_val = top2_val;
-  a.top2_idx = top2_idx;
-  a.lse = lse;
-  a.margin = margin;
-  a.chain_len = gate ? chain_len : 0;
-  a.max_ufp = gate ? repair_budget / branch_depth : 0;
-  a.tau = tau;
-  a.ufp_pos = gate ? ufp_pos : nullptr;
-  a.ufp_cnt = gate ? ufp_cnt : nullptr;
-  a.partials = reinterpret_cast<Partial*>(workspace);
-
-  const dim3 grid((unsigned)(nrow * splits)), block(kThreads);
-  hipStream_t s = as_stream(stream);
-  if (dtype == CURE_BF16) {
-    if (vec_ok) hipLaunchKernelGGL((margins_kernel<uint16_t, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((margins_kernel<uint16_t, false>), grid, block, 0, s, a);
-  } else {
-    if (vec_ok) hipLaunchKernelGGL((margins_kernel<float, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((margins_kernel<float, false>), grid, block, 0, s, a);
+extern "C" cure_status cure_margins_noalloc(const void* logits, int32_t dtype, int32_t batch,
+                                            int32_t rows, int32_t vocab, int64_t ld,
+                                            float* top1_val, int32_t* top1_idx,
+                                            float* top2_val, int32_t* top2_idx, float* lse,
+                                            float* margin, int32_t chain_len, float tau,
+                                            int32_t repair_budget, int32_t branch_depth,
+                                            int32_t* ufp_pos, int32_t* ufp_cnt, void* stream) {
+  const cure_status st = check_args(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx,
+                                    top2_val, top2_idx, lse, margin, chain_len, repair_budget,
+                                    branch_depth, ufp_pos, ufp_cnt);
+  if (st != CURE_OK || batch == 0 || rows == 0) return st;
+  const Plan pl = make_plan((int64_t)batch * rows, vocab);
+  const size_t need = pl.splits > 1 ? (size_t)batch * rows * pl.splits * sizeof(Partial) : 0;
+  if (need > kScratchBytes) return CURE_ERR_UNSUPPORTED;
+  void* ws = nullptr;
+  if (need > 0) {
+    ws = scratch_address();
+    if (!ws) return CURE_ERR_HIP;
   }
-  if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
-  if (splits > 1 || gate)
-    hipLaunchKernelGGL(margins_finish, dim3(batch), block, 0, s, a);
-  return launch_status();
+  return launch(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx, top2_val, top2_idx,
+                lse, margin, chain_len, tau, repair_budget, branch_depth, ufp_pos, ufp_cnt, pl,
+                ws, stream);
 }

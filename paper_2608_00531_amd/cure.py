@@ -40,6 +40,10 @@ _SIGNATURES = {
     "cure_margins": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64,
                                     _vp, _vp, _vp, _vp, _vp, _vp,
                                     _i32, _f32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
+    "cure_margins_noalloc_scratch_bytes": (_sz, []),
+    "cure_margins_noalloc": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64,
+                                            _vp, _vp, _vp, _vp, _vp, _vp,
+                                            _i32, _f32, _i32, _i32, _vp, _vp, _vp]),
     "cure_tree_attn_workspace_size": (_sz, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32]),
     "cure_tree_attn": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                       _i32, _f32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
@@ -158,6 +162,38 @@ def cure_margins(logits, chain_len=0, tau=float("inf"), repair_budget=0, branch_
                         chain_len, tau, repair_budget, branch_depth, _ptr(ufp_pos),
                         _ptr(ufp_cnt), _ptr(ws), wsb, _stream(dev))
     _check(st, "cure_margins")
+    return out
+
+
+def cure_margins_noalloc(logits, chain_len=0, tau=float("inf"), repair_budget=0,
+                         branch_depth=1, gate=True):
+    """As cure_margins, through the allocation-free entry point: no workspace
+    is passed; the library's fixed scratch array serves the call."""
+    _require_cuda(logits)
+    x = logits if logits.dim() == 3 else logits.unsqueeze(0)
+    if x.stride(2) != 1 or x.stride(0) != x.shape[1] * x.stride(1):
+        x = x.contiguous()
+    batch, rows, vocab = x.shape
+    dev = x.device
+    f = dict(dtype=torch.float32, device=dev)
+    i = dict(dtype=torch.int32, device=dev)
+    out = {
+        "top1_val": torch.empty(batch, rows, **f), "top1_idx": torch.empty(batch, rows, **i),
+        "top2_val": torch.empty(batch, rows, **f), "top2_idx": torch.empty(batch, rows, **i),
+        "lse": torch.empty(batch, rows, **f), "margin": torch.empty(batch, rows, **f),
+    }
+    ufp_pos = ufp_cnt = None
+    if gate:
+        ufp_pos = torch.empty(batch, chain_len, **i)
+        ufp_cnt = torch.empty(batch, **i)
+        out["ufp_pos"], out["ufp_cnt"] = ufp_pos, ufp_cnt
+    st = lib().cure_margins_noalloc(_ptr(x), _dtype_code(x), batch, rows, vocab, x.stride(1),
+                                    _ptr(out["top1_val"]), _ptr(out["top1_idx"]),
+                                    _ptr(out["top2_val"]), _ptr(out["top2_idx"]),
+                                    _ptr(out["lse"]), _ptr(out["margin"]), chain_len, tau,
+                                    repair_budget, branch_depth, _ptr(ufp_pos), _ptr(ufp_cnt),
+                                    _stream(dev))
+    _check(st, "cure_margins_noalloc")
     return out
 
 

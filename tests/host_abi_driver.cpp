@@ -48,6 +48,21 @@ int main() {
   expect(margins(1, 0, 4, 100000, 100000, P, 2, 4, I, I), CURE_OK, "margins empty");
   expect(margins(1, 1 << 20, 4096, 128256, 128256, P, 2, 4, I, I), CURE_ERR_UNSUPPORTED,
          "margins too many rows");
+  // The allocation-free entry point: the same checks, before any device call.
+  auto margins_na = [&](int dtype, int batch, int rows, int vocab, int64_t ld,
+                        const void* logits, int chain, int depth, int32_t* ufp_pos,
+                        int32_t* ufp_cnt) {
+    return (int)cure_margins_noalloc(logits, dtype, batch, rows, vocab, ld, F, I, F, I, F, F,
+                                     chain, 1.0f, 16, depth, ufp_pos, ufp_cnt, nullptr);
+  };
+  expect(margins_na(7, 1, 4, 1000, 1000, P, 2, 4, I, I), CURE_ERR_INVALID_ARG, "noalloc dtype");
+  expect(margins_na(1, 1, 4, 1000, 999, P, 2, 4, I, I), CURE_ERR_INVALID_ARG, "noalloc ld");
+  expect(margins_na(1, 1, 4, 1000, 1000, P, 2, 4, nullptr, I), CURE_ERR_INVALID_ARG,
+         "noalloc gate");
+  expect(margins_na(1, 0, 4, 100000, 100000, P, 2, 4, I, I), CURE_OK, "noalloc empty");
+  expect(margins_na(1, 1 << 20, 4096, 128256, 128256, P, 2, 4, I, I), CURE_ERR_UNSUPPORTED,
+         "noalloc too many rows");
+  expect(cure_margins_noalloc_scratch_bytes() == 256 * 1024, 1, "noalloc scratch size");
   size_t last = 0;
   for (int b : {1, 7, 16, 1024})
     for (int r : {1, 32, 48, 333})

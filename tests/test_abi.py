@@ -77,6 +77,26 @@ def test_margins_argument_errors(L):
     assert _margins(L, batch=-1) == pc.CURE_ERR_INVALID_ARG
 
 
+def test_margins_noalloc_argument_errors(L):
+    # The same host checks as cure_margins, before any device is touched.
+    def call(**kw):
+        args = dict(logits=1, dtype=1, batch=1, rows=4, vocab=100000, ld=100000,
+                    top1_val=1, top1_idx=1, top2_val=1, top2_idx=1, lse=1, margin=1,
+                    chain_len=2, tau=1.0, repair_budget=4, branch_depth=2, ufp_pos=1,
+                    ufp_cnt=1, stream=None)
+        args.update(kw)
+        return L.cure_margins_noalloc(*args.values())
+    assert call(dtype=7) == pc.CURE_ERR_INVALID_ARG
+    assert call(vocab=1, ld=1) == pc.CURE_ERR_INVALID_ARG
+    assert call(logits=None) == pc.CURE_ERR_INVALID_ARG
+    assert call(ufp_cnt=None) == pc.CURE_ERR_INVALID_ARG
+    assert call(chain_len=5) == pc.CURE_ERR_INVALID_ARG
+    assert call(rows=2000, chain_len=1500) == pc.CURE_ERR_UNSUPPORTED
+    assert call(batch=0) == pc.CURE_OK
+    assert call(batch=-1) == pc.CURE_ERR_INVALID_ARG
+    assert L.cure_margins_noalloc_scratch_bytes() == 256 * 1024
+
+
 def test_margins_workspace_size_grows_with_rows(L):
     a = L.cure_margins_workspace_size(1, 32, 128256)
     b = L.cure_margins_workspace_size(16, 48, 128256)
