@@ -130,6 +130,20 @@ CURE_DEV bool visible(int tok, int L, int N, int n, const unsigned long long (*s
   return (s_anc[n][j >> 6] >> (j & 63)) & 1ull;
 }
 
+// Additive mask of token tok for node n inside a split that ends at `end`:
+// +0 when visible() holds, -inf otherwise. Computed without branches (the
+// ancestor word is read for a clamped row index and context rows ignore it;
+// tok < end implies tok < ctx + nodes, so a row past the context is a tree
+// row), so that adding it to a score leaves no divergent write to a register
+// of an MFMA result vector.
+CURE_DEV float mask_bias(int tok, int L, int end, int n,
+                         const unsigned long long (*s_anc)[kAncWords]) {
+  const int j = min(max(tok - L, 0), CURE_MAX_TREE_NODES - 1);
+  const uint32_t bit = (uint32_t)(s_anc[n][j >> 6] >> (j & 63)) & 1u;
+  const uint32_t vis = (uint32_t)(tok < L) | ((uint32_t)(tok < end) & bit);
+  return __uint_as_float((vis ^ 1u) * 0xff800000u);
+}
+
 template <typename T>
 CURE_DEV float ld_elem(const T* p);
 template <>
@@ -315,13 +329,19 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+constexpr int kRsrcWord3 = 0x00020000;     // raw (untyped) 32-bit access, gfx9 family
 
-// A buffer resource as four wave-uniform dwords (SGPRs).
-CURE_DEV i32x4 as_i32x4(__amdgpu_buffer_rsrc_t r) {
-  i32x4 v;
-  __builtin_memcpy(&v, &r, sizeof(v));
-  return i32x4{__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
-               __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w)};
+// A raw buffer resource over `bytes` bytes at `base`, as four wave-uniform
+// dwords (SGPRs): base address (48 bits, stride 0), record count in bytes,
+// and the gfx9-family word for untyped 32-bit access. Built from integer
+// words rather than converted from the opaque resource type, which the
+// compiler would spill through a per-thread memory copy.
+CURE_DEV i32x4 raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+               __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+               __builtin_amdgcn_readfirstlane((int)bytes),
+               __builtin_amdgcn_readfirstlane(kRsrcWord3)};
 }
 
 CURE_DEV uint32_t lds_addr(const void* p) {
@@ -344,7 +364,6 @@ union Pack8 {
   i16x4 h[2];
 };
 
-constexpr int kRsrcWord3 = 0x00020000;     // raw (untyped) 32-bit access, gfx9 family
 
 // Three-input maximum as one v_max3_f32. Written as assembly because fmaxf
 // first canonicalises every operand that may be a signalling NaN (an extra
@@ -457,12 +476,6 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 
   // Buffer resources over this sequence's K and V rows (all kv-heads).
   const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.k)) + off * a.hkv * D, 0,
-      (int)seq_bytes, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.v)) + off * a.hkv * D, 0,
-      (int)seq_bytes, kRsrcWord3);
   // Per lane and DMA block: byte offset of the source chunk for tile start 0.
   uint32_t src_off[kDmaPerWave];
 #pragma unroll
@@ -481,7 +494,8 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
   // starts with s_waitcnt + barrier before any LDS read of the tile it uses.
   // A tile at or past the split's end is still issued (at an out-of-range
   // offset) so that every iteration has the same number of DMAs in flight.
-  const i32x4 rk4 = as_i32x4(rk), rv4 = as_i32x4(rv);
+  const i32x4 rk4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.k) + off * a.hkv * D, seq_bytes);
+  const i32x4 rv4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.v) + off * a.hkv * D, seq_bytes);
   auto dma_tile = [&](int buf, int t0) {
     const bool live = t0 < end;
 #pragma unroll
@@ -583,10 +597,8 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int tok = t0 + blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (!(tok < end && visible(tok, L, N, n, s_anc))) sacc[blk][r] = -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          sacc[blk][r] += mask_bias(t0 + blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3), L, end, n, s_anc);
     }
     // Row maximum: one three-input max per two scores, in two chains.
     float mb[2] = {-INFINITY, -INFINITY};
@@ -773,12 +785,6 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
   const int end = (s == S - 1) ? T : begin + a.tps;
 
   const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.k)) + off * a.hkv * D, 0,
-      (int)seq_bytes, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(reinterpret_cast<const uint16_t*>(a.v)) + off * a.hkv * D, 0,
-      (int)seq_bytes, kRsrcWord3);
   uint32_t src_off[kDmaPerWave];
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
@@ -789,7 +795,8 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
     src_off[j] = (uint32_t)((row * a.hkv + hk) * G::kRowBytes + (lchunk << 4));
   }
   const uint32_t tok_bytes = (uint32_t)(a.hkv * G::kRowBytes);
-  const i32x4 rk4 = as_i32x4(rk), rv4 = as_i32x4(rv);
+  const i32x4 rk4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.k) + off * a.hkv * D, seq_bytes);
+  const i32x4 rv4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.v) + off * a.hkv * D, seq_bytes);
   auto dma_tile = [&](int buf, int t0) {
     const bool live = t0 < end;
 #pragma unroll
@@ -881,10 +888,7 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int tok = t0 + tb * 16 + 4 * g + r;
-          if (!(tok < end && visible(tok, L, N, n, s_anc))) sacc[tb][r] = -INFINITY;
-        }
+        for (int r = 0; r < 4; ++r) sacc[tb][r] += mask_bias(t0 + tb * 16 + 4 * g + r, L, end, n, s_anc);
     }
     // Row maximum over the lane's 16 scores (eight v_max3), then its 3 partners.
     float mb = max3_raw(sacc[0][0], sacc[0][1], sacc[0][2]);
@@ -973,6 +977,340 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
       *reinterpret_cast<float4*>(a.part_o + pi * D + db * 16 + 4 * g) =
           make_float4(oacc[db][0] * inv, oacc[db][1] * inv, oacc[db][2] * inv, oacc[db][3] * inv);
     if (g == 0) a.part_lse[pi] = lse_nat;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// MFMA split kernel with RG 16-row groups per wave (v_mfma_f32_16x16x32_bf16).
+//
+// The 16-row kernel's operand layout, tile stream, tree mask and online
+// softmax, with two changes:
+//  * each wave owns RG groups of 16 query rows, and every K fragment and V^T
+//    fragment it reads from LDS feeds the MFMAs of all RG groups, so a tile's
+//    LDS reads serve 16 RG rows per wave instead of 16 (LDS read bandwidth
+//    co-bounds the K/V stream once a kv-head has more than ~128 rows);
+//  * the K/V ring holds NBUF tiles, so NBUF - 1 tiles (32 KB each at head dim
+//    128) are in flight while one is computed; only the first NDMA waves
+//    issue the tile DMA (G::kBlocks / NDMA blocks per tensor each), and the
+//    barrier after their wait releases the others.
+// Row r of a wave's group rg is query row rb * rows_per_wg + wave * 16 RG +
+// 16 rg + c (lane l = 16 g + c as in the 16-row kernel).
+template <int D, int NW, int RG, int NBUF, int NDMA, int HT, int WPE>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void tree_attn_rg(Args a) {
+  using G = TileGeo<D>;
+  constexpr int kKSteps = D / 32;                  // k-steps for Q K^T
+  constexpr int kDBlk = D / 16;                    // 16-column blocks of O^T
+  constexpr int kDmaBlocks = G::kBlocks / NDMA;    // DMA blocks per DMA wave per tensor
+  // The tile's 64 tokens are taken in HT steps of online softmax, each of
+  // kTB 16-token blocks (scores) and kPV 32-token k-steps (P V).
+  constexpr int kTB = 4 / HT;
+  constexpr int kPV = 2 / HT;
+  constexpr int kKFrags = kTB * kKSteps;           // K operand fragments per step
+  constexpr int kVFrags = kPV * kDBlk;             // V^T operand fragments per step
+  constexpr int kAheadK = 3;                       // K reads in flight ahead of their MFMAs
+  constexpr int kAheadV = 3;                       // V^T reads in flight ahead of their MFMAs
+  // Each iteration waits until its tile has landed while the NBUF - 2 tiles
+  // issued after it may still be in flight (2 instructions per block).
+  constexpr int kVmWait = waitcnt_vm((NBUF - 2) * 2 * kDmaBlocks);
+  static_assert(G::kBlocks % NDMA == 0 && NDMA <= NW, "DMA blocks split evenly over DMA waves");
+  static_assert((NBUF - 2) * 2 * kDmaBlocks < 64, "vmcnt holds 6 bits");
+  static_assert(NBUF >= 2, "a ring of at least two tiles");
+  static_assert(HT == 1 || HT == 2, "one or two softmax steps per tile");
+
+  __shared__ int s_parent[CURE_MAX_TREE_NODES];
+  __shared__ unsigned long long s_anc[CURE_MAX_TREE_NODES][kAncWords];
+  __shared__ int s_bad;
+  __shared__ __attribute__((aligned(1024))) unsigned char s_k[NBUF][G::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char s_v[NBUF][G::kTileBytes];
+
+  const int b = blockIdx.z;
+  const int hk = blockIdx.x % a.hkv;
+  const int rb = blockIdx.x / a.hkv;
+  const int s = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane & 15, g = lane >> 4;
+  const int wrow = rb * a.rows_per_wg + wave * 16 * RG;   // this wave's first row
+
+  // Query loads (they need only the launch shape) and the parent entry go out
+  // with the loads of the sequence's sizes.
+  bf16x8 qreg[RG][kKSteps];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const int R = wrow + 16 * rg + c;
+    const bool r_in = R < a.n_max * a.group;
+    const int qn = r_in ? R / a.group : 0;
+    const int qh = hk * a.group + (r_in ? R % a.group : 0);
+    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
+                           (((int64_t)b * a.n_max + qn) * a.hq + qh) * D;
+#pragma unroll
+    for (int ks = 0; ks < kKSteps; ++ks) {
+      Pack8 p;
+      p.u = r_in ? *reinterpret_cast<const uint4*>(qrow + ks * 32 + g * 8)
+                 : make_uint4(0, 0, 0, 0);
+      qreg[rg][ks] = p.v;
+    }
+  }
+  const int my_parent = tid < a.n_max ? a.parent[(int64_t)b * a.n_max + tid] : -1;
+
+  const int n_raw = a.n_nodes[b];
+  const int L = a.ctx_len[b];
+  const int64_t off = a.kv_off[b];
+  asm volatile("" : : "s"(n_raw), "s"(L), "s"(off));
+  const int N = min(n_raw, a.n_max);
+  const int T = L + N;
+  const int S = split_count(T, N, a.tps, a.max_splits);
+  const int rows = N * a.group;
+  if (S == 0) {                         // no nodes: nothing to compute; the empty tree is valid
+    report_tree(a, b, true, s == 0 && hk == 0 && rb == 0);
+    return;
+  }
+  if (s >= S || rb * a.rows_per_wg >= rows) return;
+
+  const int begin = s * a.tps;
+  const int end = (s == S - 1) ? T : begin + a.tps;
+
+  const uint32_t seq_bytes = (uint32_t)T * (uint32_t)(a.hkv * G::kRowBytes);
+  const bool dma_wave = wave < NDMA;
+  uint32_t src_off[kDmaBlocks];
+#pragma unroll
+  for (int j = 0; j < kDmaBlocks; ++j) {
+    const int byte = ((dma_wave ? wave : 0) * kDmaBlocks + j) * 1024 + lane * 16;
+    const int row = byte / G::kRowBytes;
+    const int pchunk = (byte % G::kRowBytes) >> 4;
+    const int lchunk = pchunk ^ G::swz(row);
+    src_off[j] = (uint32_t)((row * a.hkv + hk) * G::kRowBytes + (lchunk << 4));
+  }
+  const uint32_t tok_bytes = (uint32_t)(a.hkv * G::kRowBytes);
+  const i32x4 rk4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.k) + off * a.hkv * D, seq_bytes);
+  const i32x4 rv4 = raw_rsrc(reinterpret_cast<const uint16_t*>(a.v) + off * a.hkv * D, seq_bytes);
+  // Tiles at or past the split's end are still issued (at an out-of-range
+  // offset, which reads nothing) so that every iteration of a DMA wave has
+  // the same number of DMAs in flight.
+  auto dma_tile = [&](int buf, int t0) {
+    if (!dma_wave) return;
+    const bool live = t0 < end;
+#pragma unroll
+    for (int j = 0; j < kDmaBlocks; ++j) {
+      const uint32_t voff = live ? src_off[j] + (uint32_t)t0 * tok_bytes : kOobOffset;
+      const int blk = (wave * kDmaBlocks + j) * 1024;
+      dma16(lds_addr(&s_k[buf][blk]), voff, rk4);
+      dma16(lds_addr(&s_v[buf][blk]), voff, rv4);
+    }
+  };
+#pragma unroll
+  for (int i = 0; i < NBUF - 1; ++i) dma_tile(i, begin + i * kTile);
+
+  // A row block may hold fewer rows than the workgroup has row waves.
+  bool row_ok[RG];
+  int n_of[RG], head_of[RG];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    const int R = wrow + 16 * rg + c;
+    row_ok[rg] = wave * 16 * RG + 16 * rg < a.rows_per_wg && R < rows;
+    n_of[rg] = row_ok[rg] ? R / a.group : 0;
+    head_of[rg] = hk * a.group + (row_ok[rg] ? R % a.group : 0);
+  }
+  const bool wave_active = wave * 16 * RG < a.rows_per_wg && wrow < rows;
+
+  // LDS byte offsets of this lane's operands inside a tile. The swizzle takes
+  // only the row's low three bits, so a 16-row block's offset is a constant
+  // (an instruction immediate) away from the first block's.
+  int k_off[kKSteps];                              // K: row tb*16 + c, chunk 4 ks + g
+#pragma unroll
+  for (int ks = 0; ks < kKSteps; ++ks) k_off[ks] = G::offset(c, 4 * ks + g);
+  const int v_row = 4 * g + (c >> 2);
+  int v_off[kDBlk];                                // V^T: rows v_row (+16 h, +32 kt), 16-col block db
+#pragma unroll
+  for (int db = 0; db < kDBlk; ++db) v_off[db] = G::offset(v_row, 2 * db + ((c & 3) >> 1)) + (c & 1) * 8;
+
+  if (end > L) {
+    const bool ok = build_tree_loaded(N, my_parent, s_parent, s_anc, &s_bad);
+    report_tree(a, b, ok, s == S - 1 && hk == 0 && rb == 0);
+    if (!ok) {
+      __builtin_amdgcn_s_waitcnt(0);
+      return;
+    }
+  }
+
+  f32x4 oacc[RG][kDBlk];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+    for (int i = 0; i < kDBlk; ++i) oacc[rg][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[RG], l_run[RG];
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    m_run[rg] = -INFINITY;
+    l_run[rg] = 0.f;
+  }
+  const float cs = a.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // Queries and the first tiles have landed. (This also tells the compiler
+  // that no load it issued is pending, so it adds no waits inside the loop.)
+  __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg)
+    if (!row_ok[rg]) {
+#pragma unroll
+      for (int ks = 0; ks < kKSteps; ++ks) qreg[rg][ks] = bf16x8{};
+    }
+  for (int t0 = begin, buf = 0; t0 < end; t0 += kTile, buf = buf + 1 == NBUF ? 0 : buf + 1) {
+    __builtin_amdgcn_s_waitcnt(kVmWait);  // this wave's DMA into `buf` has landed
+    __syncthreads();                      // everyone's has; the previous buffer is free
+    dma_tile(buf == 0 ? NBUF - 1 : buf - 1, t0 + (NBUF - 1) * kTile);
+    if (!wave_active) continue;
+    const unsigned char* kt = s_k[buf];
+    const unsigned char* vt = s_v[buf];
+#pragma unroll
+    for (int hs = 0; hs < HT; ++hs) {
+      // Scores of this step's kTB 16-token blocks x RG row groups, each a
+      // chain of kKSteps MFMAs; every K fragment feeds all RG groups.
+      f32x4 sacc[RG][kTB];
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+        for (int tb = 0; tb < kTB; ++tb) sacc[rg][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      Pack8 kf[kKFrags];
+      auto load_k = [&](Pack8& f, int i) {
+        f.u = *reinterpret_cast<const uint4*>(kt + (hs * kTB + i % kTB) * 16 * G::kRowBytes +
+                                              k_off[i / kTB]);
+      };
+#pragma unroll
+      for (int i = 0; i < kAheadK; ++i) load_k(kf[i], i);
+#pragma unroll
+      for (int i = 0; i < kKFrags; ++i) {
+        if (i + kAheadK < kKFrags) load_k(kf[i + kAheadK], i + kAheadK);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+          sacc[rg][i % kTB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[i].v, qreg[rg][i / kTB],
+                                                                     sacc[rg][i % kTB], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, kAheadK, 0);
+#pragma unroll
+      for (int i = 0; i < kKFrags - kAheadK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, RG, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, RG * kAheadK, 0);
+      const int s0 = t0 + hs * 16 * kTB;             // first token of this step
+      if (s0 + 16 * kTB > L) {
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+          for (int tb = 0; tb < kTB; ++tb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int tok = s0 + tb * 16 + 4 * g + r;
+              sacc[rg][tb][r] += mask_bias(tok, L, end, n_of[rg], s_anc);
+            }
+      }
+      // Row maxima (the lane's 4 kTB scores, then its 3 partners), then the
+      // lazy rescale of any group whose maximum grew.
+      float m_tile[RG];
+      bool grow_any = false;
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg) {
+        float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
+#pragma unroll
+        for (int i = 3; i + 1 < 4 * kTB; i += 2)
+          mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
+        mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
+        mb = max3_raw(mb, partner<16>(mb), mb);
+        m_tile[rg] = max_halves(mb) * cs;
+        grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
+      }
+      if (__builtin_expect(__ballot(grow_any) != 0, 0)) {
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+          if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
+            const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
+            l_run[rg] *= alpha;
+#pragma unroll
+            for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
+            m_run[rg] = m_tile[rg];
+          }
+        }
+      }
+      // V^T fragment i: k-step hs * kPV + i / kDBlk, column block i % kDBlk.
+      Pack8 vf[kVFrags];
+      auto load_v = [&](Pack8& f, int i) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int rows0 = 32 * (hs * kPV + i / kDBlk) + 16 * h;   // multiple of 8: swizzle-free
+          f.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4*)(vt + rows0 * G::kRowBytes + v_off[i % kDBlk]));
+        }
+      };
+#pragma unroll
+      for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
+      bf16x8 pb[RG][kPV];
+#pragma unroll
+      for (int rg = 0; rg < RG; ++rg) {
+        const float nm = m_run[rg] == -INFINITY ? 0.f : -m_run[rg];
+        float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+        for (int kt2 = 0; kt2 < kPV; ++kt2) {
+          bf16x8 v8;
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            v8[j] = (__bf16)fast_exp2(fmaf(sacc[rg][2 * kt2 + (j >> 2)][j & 3], cs, nm));
+          pb[rg][kt2] = v8;
+          l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
+          l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
+          l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
+          l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+        }
+        l_run[rg] += l0 + l1;
+      }
+#pragma unroll
+      for (int i = 0; i < kVFrags; ++i) {
+        if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+          oacc[rg][i % kDBlk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              vf[i].v, pb[rg][i / kDBlk], oacc[rg][i % kDBlk], 0, 0, 0);
+      }
+    }
+  }
+
+  __builtin_amdgcn_s_waitcnt(0);          // the ring's trailing DMAs land before exit
+#pragma unroll
+  for (int rg = 0; rg < RG; ++rg) {
+    if (!row_ok[rg]) continue;
+    const int n = n_of[rg], head = head_of[rg];
+    float l_tot = l_run[rg] + partner<16>(l_run[rg]);
+    l_tot = sum_halves(l_tot);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lse_nat = l_tot > 0.f ? (m_run[rg] + log2f(l_tot)) * kLn2 : -INFINITY;
+    if (S == 1) {
+      const int64_t obase = (((int64_t)b * a.n_max + n) * a.hq + head) * D;
+#pragma unroll
+      for (int db = 0; db < kDBlk; ++db) {
+        const int d0 = db * 16 + 4 * g;
+        const float x0 = oacc[rg][db][0] * inv, x1 = oacc[rg][db][1] * inv;
+        const float x2 = oacc[rg][db][2] * inv, x3 = oacc[rg][db][3] * inv;
+        if (a.out_bf16) {
+          uint2 pk;
+          pk.x = pack_bf16x2(x0, x1);
+          pk.y = pack_bf16x2(x2, x3);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.o) + obase + d0) = pk;
+        } else {
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.o) + obase + d0) =
+              make_float4(x0, x1, x2, x3);
+        }
+      }
+      if (g == 0 && a.lse) a.lse[((int64_t)b * a.n_max + n) * a.hq + head] = lse_nat;
+    } else {
+      const int64_t pi = part_index(a, b, head, n, s);
+#pragma unroll
+      for (int db = 0; db < kDBlk; ++db)
+        *reinterpret_cast<float4*>(a.part_o + pi * D + db * 16 + 4 * g) =
+            make_float4(oacc[rg][db][0] * inv, oacc[rg][db][1] * inv, oacc[rg][db][2] * inv,
+                        oacc[rg][db][3] * inv);
+      if (g == 0) a.part_lse[pi] = lse_nat;
+    }
   }
 }
 
@@ -1087,6 +1425,7 @@ __global__ __launch_bounds__(256) void attn_merge(Args a) {
 struct Plan {
   bool mfma;
   bool rows16;        // MFMA kernel with 16 query rows per wave
+  bool rows48;        // MFMA kernel with three 16-row groups per wave (tree_attn_rg)
   int nw;             // waves per workgroup (MFMA kernel)
   int rows_per_wg;
   int row_blocks;
@@ -1094,17 +1433,27 @@ struct Plan {
   int max_splits;
 };
 
+// The three-row-group kernel as instantiated: 7 waves of 48 query rows (336
+// rows, one workgroup per CU with a four-tile ring), two 32-token softmax
+// steps per tile.
+constexpr int kRg3Waves = 7;
+constexpr int kRg3Rows = kRg3Waves * 48;
+
 // MFMA workgroups one CU holds at once: bounded by LDS (the K/V ring plus the
 // tree masks) and by registers (about 220 VGPRs per lane at head dim 128, so
 // two waves per SIMD; about 120 at head dim 64, four waves per SIMD).
-int mfma_wgs_per_cu(int d, int nw, bool rows16) {
+int mfma_wgs_per_cu(int d, int nw, bool rows16, bool rows48) {
+  if (rows48) return 1;
   constexpr int kLdsPerCu = 160 * 1024;
   const int stages = rows16 ? 2 : kStages;
   const int lds = 2 * stages * kTile * d * 2 +
                   CURE_MAX_TREE_NODES * (4 + kAncWords * 8) + 64;
   const int by_lds = kLdsPerCu / lds;
-  // 16-row waves hold about half the registers: four waves per SIMD.
-  const int by_regs = rows16 ? 16 / nw : (d == 128 ? 8 : 16) / nw;
+  // 16-row waves hold about half the registers: four waves per SIMD. The
+  // 8-wave 16-row kernel is planned at one workgroup per CU all the same:
+  // the longer splits halve the partial rows the merge reads, and a second
+  // workgroup per CU measured no faster.
+  const int by_regs = rows16 ? 8 / nw : (d == 128 ? 8 : 16) / nw;
   return std::max(1, std::min(by_lds, by_regs));
 }
 
@@ -1120,8 +1469,16 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   // beat the 32-row kernel's 256 + 64 split (128 vs 153 µs on the 80-node
   // sweep tree). Head dim 64: the 16-row kernel up to 128 rows, else the
   // 32-row kernel.
-  p.rows16 = mfma && (d == 128 || rows <= 128);
-  if (p.rows16) {
+  p.rows48 = mfma && d == 128 && rows > 256 && rows <= kRg3Rows;
+  p.rows16 = mfma && !p.rows48 && (d == 128 || rows <= 128);
+  if (p.rows48) {
+    // 257 - 336 rows: one block of seven 48-row waves, so each K/V tile is
+    // streamed once per kv-head (two 16-row blocks would stream it twice)
+    // and every LDS operand read feeds three row groups.
+    p.row_blocks = 1;
+    p.rows_per_wg = kRg3Rows;
+    p.nw = kRg3Waves;
+  } else if (p.rows16) {
     // Row blocks of at most 256 rows, balanced, in multiples of 16.
     p.row_blocks = (rows + 255) / 256;
     p.rows_per_wg = ((rows + p.row_blocks - 1) / p.row_blocks + 15) / 16 * 16;
@@ -1163,7 +1520,8 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
     // The shortest split (at least kMinTps tokens) whose workgroups are all
     // resident at once, so no workgroup waits for a second round. A batch with
     // more sequence x head pairs than that gets a single split per sequence.
-    const int64_t slots = (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw, p.rows16) : 2) * device_cu_count();
+    const int64_t slots =
+        (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw, p.rows16, p.rows48) : 2) * device_cu_count();
     const int64_t hi = round_tile(t_max);
     int64_t lo = round_tile(std::max<int64_t>(
         kMinTps, (t_sum * hkv * p.row_blocks + slots - 1) / std::max<int64_t>(1, slots)));
@@ -1296,7 +1654,10 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   // dispatcher spreads over the XCDs and starts together, read the heads of
   // the same token range, so concurrent reads cover whole cache rows.
   const dim3 grid(hkv * p.row_blocks, p.max_splits, batch);
-  if (p.rows16) {
+  if (p.rows48) {
+    hipLaunchKernelGGL((tree_attn_rg<128, kRg3Waves, 3, 4, 4, 2, 2>), grid, dim3(64 * kRg3Waves), 0,
+                       st, a);
+  } else if (p.rows16) {
     if (d == 128) {
       if (p.nw == 8) hipLaunchKernelGGL((tree_attn_m16<128, 8>), grid, dim3(512), 0, st, a);
       else hipLaunchKernelGGL((tree_attn_m16<128, 16>), grid, dim3(1024), 0, st, a);

@@ -107,9 +107,9 @@ def _trim_trees(w, n_nodes):
 
 
 def test_row_blocks_over_ragged_trees():
-    # 80-node trees at group 4 (320 rows: two 160-row blocks) trimmed per
-    # sequence: 160 rows (the second block has nothing to do), 68 rows, an empty
-    # tree and an empty context.
+    # 80-node trees at group 4 (320 rows: one block of seven 48-row waves)
+    # trimmed per sequence: 160 rows (waves past the tree have nothing to do),
+    # 68 rows, an empty tree and an empty context.
     say("attn row blocks ragged")
     w = make_workload("rb", batch=5, ctx_lens=[500, 1200, 30, 0, 2000], chain_len=16,
                       n_ufp=16, branch_depth=4, seed=83)
@@ -143,7 +143,7 @@ def test_largest_tree_with_gqa():
                                                   (32, 4, 128, 15, 5), (32, 8, 64, 4, 4)])
 def test_row_blocking_and_wide_trees(hq, hkv, d, n_ufp, depth):
     # Rows per kv-head = nodes x group:
-    # (32,8,128,16,4): 80 x 4 = 320 -> two 160-row blocks of the 16-row kernel;
+    # (32,8,128,16,4): 80 x 4 = 320 -> one block of the 48-row-per-wave kernel;
     # (8,8,128,16,15): 256 nodes (the maximum), G1 -> 16-row kernel, 16 waves;
     # (4,1,128,8,4): 48 x 4 = 192 -> 16-row kernel, 12 of 16 waves;
     # (4,1,64,8,4): 192 rows at head dim 64 -> 32-row kernel;
@@ -160,6 +160,29 @@ def test_row_blocking_and_wide_trees(hq, hkv, d, n_ufp, depth):
         o, lse, st = gpu_attn(w, dev, flags=flags)
         torch.cuda.synchronize()
         ref_o, ref_l = oracle_attn(w)
+        check_attn(w, o, lse, ref_o, ref_l)
+
+
+@pytest.mark.parametrize("n_ufp,depth,ctx,kv_split", [(12, 5, [300, 64], 0), (4, 17, [1000, 0], 0),
+                                                  (12, 5, [129, 2500], 3), (7, 7, [63, 700], 0),
+                                                  (12, 6, [2000, 65], 5)])
+def test_three_row_group_kernel(n_ufp, depth, ctx, kv_split):
+    # 257 - 336 rows per kv-head (group 4) take the kernel with three 16-row
+    # groups per wave: 76 nodes (304 rows), 84 (336, the block's capacity),
+    # 76 again with forced splits, 65 (260 rows, just past 256), and 88 nodes
+    # (352 rows: the 16-row kernel in two blocks) as a neighbour; the second
+    # tree is trimmed by 7 nodes so a wave's row groups end mid-node.
+    say("attn 48-row waves", n_ufp, depth, ctx, kv_split)
+    w = make_workload("r3", batch=2, hq=16, hkv=4, ctx_lens=ctx, chain_len=16, n_ufp=n_ufp,
+                      branch_depth=depth, seed=300 + n_ufp * 7 + depth)
+    n_tree = int(w.n_nodes[0])
+    _trim_trees(w, [n_tree, n_tree - 7])
+    dev = upload(w)
+    ref_o, ref_l = oracle_attn(w)
+    for flags in (0, pc.CURE_ATTN_FORCE_VALU):
+        o, lse, st = gpu_attn(w, dev, flags=flags, kv_split=kv_split)
+        torch.cuda.synchronize()
+        assert st.tolist() == [pc.CURE_OK] * w.batch
         check_attn(w, o, lse, ref_o, ref_l)
 
 
@@ -224,8 +247,8 @@ def test_long_context_full_size_sampled():
 
 
 def test_largest_sweep_tree_full_size_sampled():
-    # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, two 160-row blocks
-    # of the 16-row kernel, in the launch configuration the budget sweep times.
+    # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, one block of seven
+    # 48-row waves, in the launch configuration the budget sweep times.
     say("attn llama3_8b_ctx8k_b8_budget64 sampled")
     with Timer("generate"):
         w = preset("llama3_8b_ctx8k_b8_budget64")
@@ -235,8 +258,8 @@ def test_largest_sweep_tree_full_size_sampled():
     assert st.tolist() == [pc.CURE_OK] * w.batch
     rng = np.random.default_rng(1)
     sample = [(b, int(n)) for b in range(w.batch) for n in rng.choice(80, 2, replace=False)]
-    # Chain ends, the first node of the second row block (rows 256+ are nodes
-    # 64+ with 4 query heads per kv-head) and the last node.
+    # Chain ends, nodes whose rows straddle the waves' row groups (row 256+ is
+    # node 64+ with 4 query heads per kv-head) and the last node.
     sample += [(0, 0), (1, 15), (2, 63), (3, 64), (7, 79)]
     with Timer("oracle"):
         ref_o, ref_l = oracle_attn(w, sample=sample)

@@ -5,9 +5,11 @@ topologically ordered parent array: nested branches, wide sibling fans and
 several nodes attached straight after the context (parent -1). The interface
 takes any such array of up to 256 nodes. These cases draw random parent arrays
 of four shapes and run them through every attention kernel: the 16-row MFMA
-kernel (head dim 128 at any row count in row blocks, head dim 64 up to 128
-rows), the 32-row MFMA kernel (head dim 64 beyond 128 rows) and the vector-ALU
-kernel (bf16 forced, and fp32), against the float64 oracle element by element.
+kernel (head dim 128 up to 256 rows and, in row blocks, beyond 336; head dim 64
+up to 128 rows), the kernel with three 16-row groups per wave (head dim 128,
+257 - 336 rows), the 32-row MFMA kernel (head dim 64 beyond 128 rows) and the
+vector-ALU kernel (bf16 forced, and fp32), against the float64 oracle element
+by element.
 """
 
 import numpy as np
@@ -82,7 +84,8 @@ CASES = [
     (2, 4, 64, [100, 100], [1, 1200]),       # 400 rows at d 64: 32-row kernel
     (8, 4, 128, [24, 9], [2048, 65]),        # 96 rows, GQA 4 (the Llama shape)
     (8, 4, 128, [48, 48], [1000, 2500]),     # 192 rows
-    (8, 4, 128, [80, 61], [1300, 127]),      # 320 rows: two row blocks
+    (8, 4, 128, [80, 61], [1300, 127]),      # 320 rows: 48-row waves
+    (2, 4, 128, [84, 70], [500, 3000]),      # 336 rows: the 48-row block's capacity
     (4, 8, 128, [32, 17], [900, 4000]),      # 256 rows at GQA 8
     (2, 1, 64, [200, 3], [500, 63]),         # 200 rows at d 64 and GQA 1
     (1, 8, 64, [16, 12], [128, 129]),        # 128 rows at d 64: 16-row kernel
