@@ -187,3 +187,53 @@ def test_ufp_worked_example_and_edges():
     assert oracle.ufp_select(m, -np.inf, 100, 1) == []
     assert oracle.ufp_select(m, 1.0, 3, 4) == []               # a whole branch does not fit
     assert oracle.ufp_select(m, np.inf, 100, 1) == [2, 0, 3, 4, 1]
+
+
+def test_margins_invariant_under_permutation_of_positions():
+    # Eq. 2 reads a row as a multiset of (position, value): permuting the
+    # positions of a tie-free row leaves the top-1/top-2 values, the margin and
+    # the log-sum-exp unchanged and moves the reported indices with it.
+    rng = np.random.default_rng(21)
+    for vocab in (2, 3, 17, 256, 5000):
+        for _ in range(6):
+            row = rng.permutation(np.linspace(-6.0, 9.0, vocab)).astype(np.float32)
+            perm = rng.permutation(vocab)
+            moved = row[perm]                       # moved[j] = row[perm[j]]
+            inv = np.empty(vocab, np.int64)
+            inv[perm] = np.arange(vocab)
+            a = oracle.margins(row[None, :], "f32")
+            b = oracle.margins(moved[None, :], "f32")
+            assert b["top1_val"][0] == a["top1_val"][0] and b["top2_val"][0] == a["top2_val"][0]
+            assert b["margin"][0] == a["margin"][0]
+            assert b["lse"][0] == pytest.approx(a["lse"][0], abs=1e-12)
+            assert b["top1_idx"][0] == inv[a["top1_idx"][0]]
+            assert b["top2_idx"][0] == inv[a["top2_idx"][0]]
+
+
+def subset_brute_ufp(m, tau, budget, depth):
+    """Over every subset of the candidate positions (margin < tau) that fits
+    the budget in whole branches, the best is the largest one whose entries,
+    listed in ascending (margin, position) order, are lexicographically
+    smallest; returned in that order."""
+    cand = [i for i in range(len(m)) if m[i] < tau]
+    best = None
+    for k in range(len(cand) + 1):
+        if k * depth > budget:
+            break
+        for sub in itertools.combinations(cand, k):
+            key = sorted((float(m[i]), i) for i in sub)
+            if best is None or len(key) > len(best) or (len(key) == len(best) and key < best):
+                best = key
+    return [i for _, i in best]
+
+
+def test_ufp_against_subset_brute_force():
+    rng = np.random.default_rng(8)
+    levels = np.array([0.1, 0.5, 0.5, 0.9, 1.0, 1.5, 3.0], np.float32)
+    for _ in range(400):
+        K = int(rng.integers(1, 9))
+        m = rng.choice(levels, size=K)
+        tau = float(rng.choice([0.0, 0.5, 1.0, 2.0, np.inf]))
+        budget = int(rng.integers(0, 24))
+        depth = int(rng.integers(1, 5))
+        assert oracle.ufp_select(m, tau, budget, depth) == subset_brute_ufp(m, tau, budget, depth)
