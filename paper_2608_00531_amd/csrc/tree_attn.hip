@@ -1513,29 +1513,44 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
     }
     return c * hkv * p.row_blocks;
   };
+  const int64_t slots =
+      (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw, p.rows16, p.rows48) : 2) * device_cu_count();
+  // The shortest split (at least kMinTps tokens) whose workgroups are all
+  // resident at once, so no workgroup waits for a second round. A batch with
+  // more sequence x head pairs than that gets a single split per sequence.
+  const auto shortest_resident_split = [&]() {
+    const int64_t hi = round_tile(t_max);
+    const int64_t lo = round_tile(std::max<int64_t>(
+        kMinTps, (t_sum * hkv * p.row_blocks + slots - 1) / std::max<int64_t>(1, slots)));
+    if (lo >= hi || workgroups(hi) > slots) return hi;
+    // workgroups() falls as tps grows: bisect over multiples of the tile.
+    int64_t a = lo / kTile, z = hi / kTile;         // workgroups(z * kTile) <= slots
+    while (a < z) {
+      const int64_t m = (a + z) / 2;
+      if (workgroups(m * kTile) <= slots) z = m;
+      else a = m + 1;
+    }
+    return z * kTile;
+  };
   int64_t tps;
   if (kv_split > 0) {
     tps = round_tile((t_max + kv_split - 1) / kv_split);
   } else {
-    // The shortest split (at least kMinTps tokens) whose workgroups are all
-    // resident at once, so no workgroup waits for a second round. A batch with
-    // more sequence x head pairs than that gets a single split per sequence.
-    const int64_t slots =
-        (int64_t)(mfma ? mfma_wgs_per_cu(d, p.nw, p.rows16, p.rows48) : 2) * device_cu_count();
-    const int64_t hi = round_tile(t_max);
-    int64_t lo = round_tile(std::max<int64_t>(
-        kMinTps, (t_sum * hkv * p.row_blocks + slots - 1) / std::max<int64_t>(1, slots)));
-    if (lo >= hi || workgroups(hi) > slots) {
-      tps = hi;
-    } else {
-      // workgroups() falls as tps grows: bisect over multiples of the tile.
-      int64_t a = lo / kTile, z = hi / kTile;       // workgroups(z * kTile) <= slots
-      while (a < z) {
-        const int64_t m = (a + z) / 2;
-        if (workgroups(m * kTile) <= slots) z = m;
-        else a = m + 1;
+    tps = shortest_resident_split();
+    // A small launch (even the shortest splits leave most CUs idle, as for one
+    // sequence) cuts the 16-row kernel's rows into more blocks, of at least 32
+    // rows: the blocks of one kv-head and split are hkv workgroup ids apart,
+    // so they share an XCD's L2 for the K/V stream, and more CUs stream it
+    // (one sequence at 128 rows: 72 -> 216 workgroups).
+    const int64_t fits = slots / std::max<int64_t>(1, workgroups(tps));
+    if (p.rows16 && fits >= 2 && rows >= 64) {
+      const int blocks = (int)std::min<int64_t>((int64_t)p.row_blocks * fits, rows / 32);
+      if (blocks > p.row_blocks) {
+        p.rows_per_wg = ((rows + blocks - 1) / blocks + 15) / 16 * 16;
+        p.row_blocks = (rows + p.rows_per_wg - 1) / p.rows_per_wg;
+        p.nw = p.rows_per_wg > 128 ? 16 : 8;
+        tps = shortest_resident_split();
       }
-      tps = z * kTile;
     }
   }
   // Splits index the grid's y dimension (at most kMaxGridY).
