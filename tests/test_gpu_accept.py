@@ -101,3 +101,20 @@ def test_random_batches(seed):
         assert int(got["resync"][b]) == ref["resync"]
         p = got["path"][b].tolist()
         assert p[: ref["acc_len"]] == ref["path"] and all(x == -1 for x in p[ref["acc_len"]:])
+
+
+def test_sweep_mean_accepted_chain_closed_form():
+    # The sweep's E[a] estimate (cure_accept over 2048 seeded trees) at budget
+    # 0, a pure 16-node chain agreeing i.i.d. with probability 0.8: the
+    # accepted length is the run of leading agreements, E[a] = sum_k 0.8^k.
+    import os
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    import bench
+    say("accept sweep E[a] closed form")
+    mean, se, resync = bench.mean_accepted(pc, torch, 0, 2048, 0)
+    closed = sum(0.8 ** k for k in range(1, 17))
+    assert abs(mean - closed) < 4 * se, (mean, se, closed)
+    assert resync == 0.0                 # a chain has no repair node to resync

@@ -112,3 +112,25 @@ def test_rate_table_ties_go_to_the_smaller_budget():
              "margins_us": 0.0, "accept_us": 0.0} for b in (0, 8)]
     _, best = bench.rate_table(rows, 10.0, 1, 1, ratios=(1.0,))
     assert best["cd_1_x_weights"]["budget"] == 0
+
+
+def test_chain_acceptance_matches_geometric_closed_form():
+    # The sweep's E[a] at budget 0: a pure 16-node chain whose nodes agree with
+    # the synthetic target i.i.d. with probability p. The accepted length is the
+    # number of leading agreements (Eq. 1), so E[a] = sum_{k=1..16} p^k, 3.887
+    # at p = 0.8. The acceptance here is the oracle's; the GPU estimate the
+    # sweep reports is checked against the same closed form in the GPU tests.
+    import math
+    import numpy as np
+    import oracle
+    from synth import make_workload
+    n, p = 3000, 0.8
+    w = make_workload("chain", dtype="f32", batch=n, hq=1, hkv=1, d=4, vocab=64,
+                      ctx_lens=[1] * n, chain_len=16, n_ufp=0, branch_depth=4, seed=901,
+                      p_agree=p)
+    acc = np.array([oracle.accept(w.parent[b], w.token[b], w.tgt_planted[b], int(w.root_tgt[b]),
+                                  int(w.n_nodes[b]), w.chain_len)["acc_len"] for b in range(n)])
+    closed = sum(p ** k for k in range(1, 17))
+    assert closed == pytest.approx(p * (1 - p ** 16) / (1 - p))
+    se = acc.std() / math.sqrt(n)
+    assert abs(acc.mean() - closed) < 4 * se
