@@ -123,6 +123,50 @@ def test_row_blocks_over_ragged_trees():
         check_attn(w, o, lse, ref_o, ref_l)
 
 
+def _seg_batch(seed=87):
+    # Twenty sequences of very different lengths, with an empty context,
+    # contexts shorter than a tile, empty trees in the middle and at the end
+    # and a one-node tree: a launch whose splits are limited by the workgroups
+    # the GPU holds at once, so most sequences get splits of different counts
+    # and the last split of each is short.
+    rng = np.random.default_rng(5)
+    ctx = [int(x) for x in rng.integers(0, 4000, 20)]
+    ctx[3], ctx[7], ctx[11] = 0, 5, 63
+    nn = [8] * 20
+    nn[5], nn[19], nn[12] = 0, 0, 1
+    w = make_workload("seg", batch=20, ctx_lens=ctx, chain_len=8, n_ufp=0, branch_depth=1,
+                      seed=seed)
+    _trim_trees(w, nn)
+    return w
+
+
+def test_split_limited_ragged_batch():
+    say("attn split-limited ragged batch")
+    w = _seg_batch()
+    dev = upload(w)
+    ref_o, ref_l = oracle_attn(w)
+    for kv_split in (0, 5):                     # planned splits, then 5 forced
+        o, lse, st = gpu_attn(w, dev, kv_split=kv_split)
+        torch.cuda.synchronize()
+        assert st.tolist() == [pc.CURE_OK] * w.batch
+        check_attn(w, o, lse, ref_o, ref_l)
+
+
+def test_split_limited_batch_reports_a_malformed_tree():
+    say("attn split-limited ragged batch, malformed tree")
+    w = _seg_batch(seed=88)
+    w.parent[8, 3] = 5                           # a parent after its child
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev)
+    torch.cuda.synchronize()
+    want = [pc.CURE_OK] * w.batch
+    want[8] = pc.CURE_ERR_BAD_TREE
+    assert st.tolist() == want
+    keep = [(b, n) for b in range(w.batch) if b != 8 for n in range(int(w.n_nodes[b]))]
+    ref_o, ref_l = oracle_attn(w, sample=keep)
+    check_attn(w, o, lse, ref_o, ref_l, sample=keep)
+
+
 def test_largest_tree_with_gqa():
     # 256 nodes (the maximum) at group 4: 1024 rows per kv-head, four 256-row blocks.
     say("attn 256 nodes x group 4")
