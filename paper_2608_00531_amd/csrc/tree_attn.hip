@@ -1465,10 +1465,11 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   const int group = hq / hkv;
   const int rows = n_max * group;
   // Head dim 128: the 16-row kernel, in balanced row blocks of at most 256
-  // rows (8 waves up to 128 rows, else 16). At 320 rows two 160-row blocks
-  // beat the 32-row kernel's 256 + 64 split (128 vs 153 µs on the 80-node
-  // sweep tree). Head dim 64: the 16-row kernel up to 128 rows, else the
-  // 32-row kernel.
+  // rows (8 waves up to 128 rows, else 16), except for 257 - 336 rows, which
+  // one workgroup of the three-row-group kernel covers (on the 80-node sweep
+  // tree it beats two 160-row blocks of the 16-row kernel, 115 vs 122 µs,
+  // which beat the 32-row kernel's 256 + 64 split, 153 µs). Head dim 64: the
+  // 16-row kernel up to 128 rows, else the 32-row kernel.
   p.rows48 = mfma && d == 128 && rows > 256 && rows <= kRg3Rows;
   p.rows16 = mfma && !p.rows48 && (d == 128 || rows <= 128);
   if (p.rows48) {
