@@ -70,3 +70,45 @@ def test_graph_replays_match_eager():
             for key in ("acc_len", "path", "best", "bonus", "resync"):
                 assert torch.equal(cap[2][key], eager[2][key]), (rep, key)
             del junk
+
+
+def test_graph_replays_ragged_batch_with_repair():
+    # The ragged 16-sequence batch (two context splits, the merge launch, the
+    # UFP gate on unsplit rows) and the repair-tree builder fed the captured
+    # margins, all in one graph: every replay, after eager work, reproduces
+    # the eager results bit for bit.
+    say("step graph replay, ragged batch + repair")
+    w = preset("llama3_8b_ragged_b16")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dev = upload(w)
+        chain_tok = dev["token"][:, : w.chain_len].contiguous()
+
+        def step():
+            m, att, acc = run_step(w, dev)
+            rep = pc.cure_repair_tree(dev["logits"], m["margin"], m["ufp_pos"], m["ufp_cnt"],
+                                      chain_tok, w.repair_budget, w.branch_depth, w.tau)
+            return m, att, acc, rep
+
+        eager = step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            cap = step()
+        for rep_i in range(3):
+            junk = torch.randn(1 << 20, device="cuda").sum()
+            torch.cuda.synchronize()
+            cap[0]["top1_idx"].fill_(-7)
+            cap[1][0].zero_()
+            cap[2]["acc_len"].fill_(-7)
+            cap[3]["parent"].fill_(-7)
+            g.replay()
+            torch.cuda.synchronize()
+            for key in ("top1_idx", "top2_idx", "margin", "lse", "ufp_pos", "ufp_cnt"):
+                assert torch.equal(cap[0][key], eager[0][key]), (rep_i, key)
+            assert torch.equal(cap[1][0], eager[1][0]) and torch.equal(cap[1][1], eager[1][1])
+            for key in ("acc_len", "path", "best", "bonus", "resync"):
+                assert torch.equal(cap[2][key], eager[2][key]), (rep_i, key)
+            for key in ("parent", "token", "n_nodes", "branch_cnt"):
+                assert torch.equal(cap[3][key], eager[3][key]), (rep_i, key)
+            del junk
