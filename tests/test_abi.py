@@ -257,3 +257,35 @@ def test_read_ceiling_argument_errors(L):
     assert L.cure_read_ceiling(None, 64, 1, None) == pc.CURE_ERR_INVALID_ARG
     assert L.cure_read_ceiling(1, 64, None, None) == pc.CURE_ERR_INVALID_ARG
     assert L.cure_read_ceiling(1, 60, 1, None) == pc.CURE_ERR_INVALID_ARG  # not 16-byte multiple
+
+
+def _attn_ws(L, ctx, nn, hq=32, hkv=8, d=128, n_max=32, kv_split=0):
+    c = np.ascontiguousarray(ctx, np.int32)
+    n = np.ascontiguousarray(nn, np.int32)
+    return L.cure_tree_attn_workspace_size(len(c), hq, hkv, d, n_max,
+                                           c.ctypes.data_as(ctypes.c_void_p),
+                                           n.ctypes.data_as(ctypes.c_void_p), kv_split)
+
+
+def _partials_bytes(batch, hq, n_max, splits, d):
+    rows = batch * hq * n_max * splits                  # fp32 rows, then their LSEs,
+    up = lambda x: (x + 255) // 256 * 256               # each array 256-byte aligned
+    return up(rows * d * 4) + up(rows * 4)
+
+
+def test_automatic_split_plan_hand_worked(L):
+    # The split plan of the 256-CU GPU, worked by hand: the shortest split (a
+    # multiple of the 64-token tile, at least 256 tokens) whose workgroups
+    # (splits x kv-heads x row blocks, one per CU) are all resident at once.
+    # One sequence, 2048 + 32 tokens: 8 kv-heads fit 32 splits, so 256-token
+    # splits, ceil(2080 / 256) = 9 of them.
+    assert _attn_ws(L, [2048], [32]) == _partials_bytes(1, 32, 32, 9, 128)
+    # Four sequences of 32768 + 32 tokens: 32 workgroups per split index, so 8
+    # splits per sequence, ceil(32800 / 8) = 4100 -> 4160 tokens.
+    assert _attn_ws(L, [32768] * 4, [32] * 4) == _partials_bytes(4, 32, 32, 8, 128)
+    # Forced splits: ceil(2080 / 3) = 694 -> 704-token splits, 3 of them.
+    assert _attn_ws(L, [2048], [32], kv_split=3) == _partials_bytes(1, 32, 32, 3, 128)
+    # A sequence that fits one split needs no partials at all.
+    assert _attn_ws(L, [100, 200], [8, 8], kv_split=1) == 0
+    # No sequence with tree nodes: nothing to plan.
+    assert _attn_ws(L, [500, 700], [0, 0]) == 0
