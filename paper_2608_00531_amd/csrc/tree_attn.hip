@@ -1420,6 +1420,14 @@ __global__ __launch_bounds__(256) void attn_merge(Args a) {
       wsum > 0.f ? m + logf(wsum) : -INFINITY;
 }
 
+// Status of a launch with no tree nodes at all: every sequence's (empty)
+// tree is valid. A fill kernel rather than a memset, so that the call stays
+// capturable in a graph.
+__global__ __launch_bounds__(256) void tree_status_ok(int32_t* status, int batch) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < batch) status[i] = CURE_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Host-side plan: tokens per split and the launch shape.
 struct Plan {
@@ -1606,7 +1614,15 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   if (hq % hkv != 0) return CURE_ERR_INVALID_ARG;
   if (d != 64 && d != 128) return CURE_ERR_UNSUPPORTED;
   if (n_max > CURE_MAX_TREE_NODES) return CURE_ERR_UNSUPPORTED;
-  if (batch == 0 || n_max == 0) return CURE_OK;
+  if (batch == 0) return CURE_OK;
+  if (n_max == 0) {                     // no sequence can have nodes
+    if (tree_status) {
+      hipLaunchKernelGGL(tree_status_ok, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0,
+                         as_stream(stream), tree_status, batch);
+      return launch_status();
+    }
+    return CURE_OK;
+  }
   if (!q || !k || !v || !o || !kv_off || !ctx_len || !n_nodes || !parent || !host_ctx_len ||
       !host_n_nodes)
     return CURE_ERR_INVALID_ARG;
@@ -1623,7 +1639,14 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
     if ((t_max + kTile) * hkv * d * 2 >= (int64_t(1) << 31)) mfma = false;
   }
   const Plan p = make_plan(batch, hq, hkv, d, n_max, host_ctx_len, host_n_nodes, kv_split, mfma);
-  if (p.max_splits == 0) return CURE_OK;    // no sequence has tree nodes
+  if (p.max_splits == 0) {              // no sequence has tree nodes
+    if (tree_status) {
+      hipLaunchKernelGGL(tree_status_ok, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0,
+                         as_stream(stream), tree_status, batch);
+      return launch_status();
+    }
+    return CURE_OK;
+  }
   const size_t need = plan_workspace(p, batch, hq, d, n_max);
   if (need > 0 && (!workspace || workspace_bytes < need)) return CURE_ERR_WORKSPACE;
   if ((size_t)p.row_blocks * hkv > 65535 || batch > 65535) return CURE_ERR_UNSUPPORTED;

@@ -7,6 +7,8 @@ context and 256-node trees; row blocking beyond one workgroup; head dim 64;
 malformed trees; and the full-size long-context workload on sampled nodes.
 """
 
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -165,6 +167,32 @@ def test_split_limited_batch_reports_a_malformed_tree():
     keep = [(b, n) for b in range(w.batch) if b != 8 for n in range(int(w.n_nodes[b]))]
     ref_o, ref_l = oracle_attn(w, sample=keep)
     check_attn(w, o, lse, ref_o, ref_l, sample=keep)
+
+
+def test_no_tree_nodes_anywhere_reports_every_tree_valid():
+    # A launch in which no sequence has tree nodes computes nothing, yet every
+    # sequence's (empty) tree is valid and its status must say so.
+    say("attn no tree nodes")
+    w = make_workload("empty", batch=3, ctx_lens=[100, 0, 70], chain_len=4, n_ufp=0,
+                      branch_depth=1, seed=95)
+    _trim_trees(w, [0, 0, 0])
+    dev = upload(w)
+    L = pc.lib()
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None
+    hc = np.ascontiguousarray(w.ctx_len, np.int32)
+    hn = np.ascontiguousarray(w.n_nodes, np.int32)
+    o = torch.empty(w.batch, w.n_max, w.hq, w.d, dtype=torch.bfloat16, device="cuda")
+    for flags, n_max in ((0, w.n_max), (pc.CURE_ATTN_FORCE_VALU, w.n_max), (0, 0)):
+        status = torch.full((w.batch,), -7, dtype=torch.int32, device="cuda")
+        st = L.cure_tree_attn(ptr(dev["q"]), ptr(dev["k"]), ptr(dev["v"]), ptr(o), None,
+                              pc.CURE_BF16, pc.CURE_BF16, w.batch, w.hq, w.hkv, w.d, w.scale,
+                              ptr(dev["kv_off"]), ptr(dev["ctx_len"]), ptr(dev["n_nodes"]),
+                              ptr(dev["parent"]), n_max, hc.ctypes.data_as(ctypes.c_void_p),
+                              hn.ctypes.data_as(ctypes.c_void_p), 0, flags, ptr(status), None, 0,
+                              ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        torch.cuda.synchronize()
+        assert st == pc.CURE_OK
+        assert status.tolist() == [pc.CURE_OK] * w.batch, (flags, n_max)
 
 
 def test_largest_tree_with_gqa():
