@@ -28,6 +28,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 #include <vector>
 
 #include "common.hpp"
@@ -993,8 +994,14 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
 //    128) are in flight while one is computed; only the first NDMA waves
 //    issue the tile DMA (G::kBlocks / NDMA blocks per tensor each), and the
 //    barrier after their wait releases the others.
-// Row r of a wave's group rg is query row rb * rows_per_wg + wave * 16 RG +
-// 16 rg + c (lane l = 16 g + c as in the 16-row kernel).
+// The block's ceil(rows_per_wg / 16) row groups are dealt so that the first
+// n_full waves own RG groups each and the others RG - 1: waves w and w + 4
+// share a SIMD, so with 8 waves every SIMD carries the same number of groups
+// whenever the count allows (320 rows: 3 + 2 groups on each SIMD, where seven
+// 3-group waves put 6 groups on three SIMDs and 3 on the fourth). A wave
+// runs the tile loop's body instantiated for its own group count. Row r of a
+// wave's group rg is query row rb * rows_per_wg + 16 (first + rg) + c, with
+// first the wave's first group (lane l = 16 g + c as in the 16-row kernel).
 template <int D, int NW, int RG, int NBUF, int NDMA, int HT, int WPE>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void tree_attn_rg(Args a) {
@@ -1030,7 +1037,11 @@ void tree_attn_rg(Args a) {
   const int s = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
-  const int wrow = rb * a.rows_per_wg + wave * 16 * RG;   // this wave's first row
+  const int groups_wg = (a.rows_per_wg + 15) / 16;
+  const int n_full = min(NW, max(0, groups_wg - (RG - 1) * NW));
+  const int my_groups = wave < n_full ? RG : RG - 1;
+  const int first = wave < n_full ? RG * wave : RG * n_full + (RG - 1) * (wave - n_full);
+  const int wrow = rb * a.rows_per_wg + 16 * first;        // this wave's first row
 
   // Query loads (they need only the launch shape) and the parent entry go out
   // with the loads of the sequence's sizes.
@@ -1038,7 +1049,7 @@ void tree_attn_rg(Args a) {
 #pragma unroll
   for (int rg = 0; rg < RG; ++rg) {
     const int R = wrow + 16 * rg + c;
-    const bool r_in = R < a.n_max * a.group;
+    const bool r_in = rg < my_groups && R < a.n_max * a.group;
     const int qn = r_in ? R / a.group : 0;
     const int qh = hk * a.group + (r_in ? R % a.group : 0);
     const uint16_t* qrow = reinterpret_cast<const uint16_t*>(a.q) +
@@ -1107,11 +1118,11 @@ void tree_attn_rg(Args a) {
 #pragma unroll
   for (int rg = 0; rg < RG; ++rg) {
     const int R = wrow + 16 * rg + c;
-    row_ok[rg] = wave * 16 * RG + 16 * rg < a.rows_per_wg && R < rows;
+    row_ok[rg] = rg < my_groups && 16 * (first + rg) < a.rows_per_wg && R < rows;
     n_of[rg] = row_ok[rg] ? R / a.group : 0;
     head_of[rg] = hk * a.group + (row_ok[rg] ? R % a.group : 0);
   }
-  const bool wave_active = wave * 16 * RG < a.rows_per_wg && wrow < rows;
+  const bool wave_active = my_groups > 0 && 16 * first < a.rows_per_wg && wrow < rows;
 
   // LDS byte offsets of this lane's operands inside a tile. The swizzle takes
   // only the row's low three bits, so a 16-row block's offset is a constant
@@ -1163,116 +1174,122 @@ void tree_attn_rg(Args a) {
     if (!wave_active) continue;
     const unsigned char* kt = s_k[buf];
     const unsigned char* vt = s_v[buf];
-#pragma unroll
-    for (int hs = 0; hs < HT; ++hs) {
-      // Scores of this step's kTB 16-token blocks x RG row groups, each a
-      // chain of kKSteps MFMAs; every K fragment feeds all RG groups.
-      f32x4 sacc[RG][kTB];
-#pragma unroll
-      for (int rg = 0; rg < RG; ++rg)
-#pragma unroll
-        for (int tb = 0; tb < kTB; ++tb) sacc[rg][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      Pack8 kf[kKFrags];
-      auto load_k = [&](Pack8& f, int i) {
-        f.u = *reinterpret_cast<const uint4*>(kt + (hs * kTB + i % kTB) * 16 * G::kRowBytes +
-                                              k_off[i / kTB]);
-      };
-#pragma unroll
-      for (int i = 0; i < kAheadK; ++i) load_k(kf[i], i);
-#pragma unroll
-      for (int i = 0; i < kKFrags; ++i) {
-        if (i + kAheadK < kKFrags) load_k(kf[i + kAheadK], i + kAheadK);
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-          sacc[rg][i % kTB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[i].v, qreg[rg][i / kTB],
-                                                                     sacc[rg][i % kTB], 0, 0, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x100, kAheadK, 0);
-#pragma unroll
-      for (int i = 0; i < kKFrags - kAheadK; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, RG, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, RG * kAheadK, 0);
-      const int s0 = t0 + hs * 16 * kTB;             // first token of this step
-      if (s0 + 16 * kTB > L) {
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-#pragma unroll
-          for (int tb = 0; tb < kTB; ++tb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int tok = s0 + tb * 16 + 4 * g + r;
-              sacc[rg][tb][r] += mask_bias(tok, L, end, n_of[rg], s_anc);
+    // The tile's work for NG row groups (NG = RG or RG - 1, this wave's count).
+    auto tile_body = [&](auto ng) {
+      constexpr int NG = decltype(ng)::value;
+  #pragma unroll
+      for (int hs = 0; hs < HT; ++hs) {
+        // Scores of this step's kTB 16-token blocks x NG row groups, each a
+        // chain of kKSteps MFMAs; every K fragment feeds all NG groups.
+        f32x4 sacc[NG][kTB];
+  #pragma unroll
+        for (int rg = 0; rg < NG; ++rg)
+  #pragma unroll
+          for (int tb = 0; tb < kTB; ++tb) sacc[rg][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        Pack8 kf[kKFrags];
+        auto load_k = [&](Pack8& f, int i) {
+          f.u = *reinterpret_cast<const uint4*>(kt + (hs * kTB + i % kTB) * 16 * G::kRowBytes +
+                                                k_off[i / kTB]);
+        };
+  #pragma unroll
+        for (int i = 0; i < kAheadK; ++i) load_k(kf[i], i);
+  #pragma unroll
+        for (int i = 0; i < kKFrags; ++i) {
+          if (i + kAheadK < kKFrags) load_k(kf[i + kAheadK], i + kAheadK);
+  #pragma unroll
+          for (int rg = 0; rg < NG; ++rg)
+            sacc[rg][i % kTB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[i].v, qreg[rg][i / kTB],
+                                                                       sacc[rg][i % kTB], 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, kAheadK, 0);
+  #pragma unroll
+        for (int i = 0; i < kKFrags - kAheadK; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NG, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NG * kAheadK, 0);
+        const int s0 = t0 + hs * 16 * kTB;             // first token of this step
+        if (s0 + 16 * kTB > L) {
+  #pragma unroll
+          for (int rg = 0; rg < NG; ++rg)
+  #pragma unroll
+            for (int tb = 0; tb < kTB; ++tb)
+  #pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int tok = s0 + tb * 16 + 4 * g + r;
+                sacc[rg][tb][r] += mask_bias(tok, L, end, n_of[rg], s_anc);
+              }
+        }
+        // Row maxima (the lane's 4 kTB scores, then its 3 partners), then the
+        // lazy rescale of any group whose maximum grew.
+        float m_tile[NG];
+        bool grow_any = false;
+  #pragma unroll
+        for (int rg = 0; rg < NG; ++rg) {
+          float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
+  #pragma unroll
+          for (int i = 3; i + 1 < 4 * kTB; i += 2)
+            mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
+          mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
+          mb = max3_raw(mb, partner<16>(mb), mb);
+          m_tile[rg] = max_halves(mb) * cs;
+          grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
+        }
+        if (__builtin_expect(__ballot(grow_any) != 0, 0)) {
+  #pragma unroll
+          for (int rg = 0; rg < NG; ++rg) {
+            if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
+              const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
+              l_run[rg] *= alpha;
+  #pragma unroll
+              for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
+              m_run[rg] = m_tile[rg];
             }
-      }
-      // Row maxima (the lane's 4 kTB scores, then its 3 partners), then the
-      // lazy rescale of any group whose maximum grew.
-      float m_tile[RG];
-      bool grow_any = false;
-#pragma unroll
-      for (int rg = 0; rg < RG; ++rg) {
-        float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
-#pragma unroll
-        for (int i = 3; i + 1 < 4 * kTB; i += 2)
-          mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
-        mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
-        mb = max3_raw(mb, partner<16>(mb), mb);
-        m_tile[rg] = max_halves(mb) * cs;
-        grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
-      }
-      if (__builtin_expect(__ballot(grow_any) != 0, 0)) {
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg) {
-          if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
-            const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
-            l_run[rg] *= alpha;
-#pragma unroll
-            for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
-            m_run[rg] = m_tile[rg];
           }
         }
-      }
-      // V^T fragment i: k-step hs * kPV + i / kDBlk, column block i % kDBlk.
-      Pack8 vf[kVFrags];
-      auto load_v = [&](Pack8& f, int i) {
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int rows0 = 32 * (hs * kPV + i / kDBlk) + 16 * h;   // multiple of 8: swizzle-free
-          f.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(vt + rows0 * G::kRowBytes + v_off[i % kDBlk]));
+        // V^T fragment i: k-step hs * kPV + i / kDBlk, column block i % kDBlk.
+        Pack8 vf[kVFrags];
+        auto load_v = [&](Pack8& f, int i) {
+  #pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int rows0 = 32 * (hs * kPV + i / kDBlk) + 16 * h;   // multiple of 8: swizzle-free
+            f.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_i16x4*)(vt + rows0 * G::kRowBytes + v_off[i % kDBlk]));
+          }
+        };
+  #pragma unroll
+        for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
+        bf16x8 pb[NG][kPV];
+  #pragma unroll
+        for (int rg = 0; rg < NG; ++rg) {
+          const float nm = m_run[rg] == -INFINITY ? 0.f : -m_run[rg];
+          float l0 = 0.f, l1 = 0.f;
+  #pragma unroll
+          for (int kt2 = 0; kt2 < kPV; ++kt2) {
+            bf16x8 v8;
+  #pragma unroll
+            for (int j = 0; j < 8; ++j)
+              v8[j] = (__bf16)fast_exp2(fmaf(sacc[rg][2 * kt2 + (j >> 2)][j & 3], cs, nm));
+            pb[rg][kt2] = v8;
+            l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
+            l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
+            l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
+            l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+          }
+          l_run[rg] += l0 + l1;
         }
-      };
-#pragma unroll
-      for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
-      bf16x8 pb[RG][kPV];
-#pragma unroll
-      for (int rg = 0; rg < RG; ++rg) {
-        const float nm = m_run[rg] == -INFINITY ? 0.f : -m_run[rg];
-        float l0 = 0.f, l1 = 0.f;
-#pragma unroll
-        for (int kt2 = 0; kt2 < kPV; ++kt2) {
-          bf16x8 v8;
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            v8[j] = (__bf16)fast_exp2(fmaf(sacc[rg][2 * kt2 + (j >> 2)][j & 3], cs, nm));
-          pb[rg][kt2] = v8;
-          l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
-          l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
-          l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
-          l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+  #pragma unroll
+        for (int i = 0; i < kVFrags; ++i) {
+          if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
+  #pragma unroll
+          for (int rg = 0; rg < NG; ++rg)
+            oacc[rg][i % kDBlk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                vf[i].v, pb[rg][i / kDBlk], oacc[rg][i % kDBlk], 0, 0, 0);
         }
-        l_run[rg] += l0 + l1;
       }
-#pragma unroll
-      for (int i = 0; i < kVFrags; ++i) {
-        if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-          oacc[rg][i % kDBlk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              vf[i].v, pb[rg][i / kDBlk], oacc[rg][i % kDBlk], 0, 0, 0);
-      }
-    }
+    };
+    if (my_groups == RG) tile_body(std::integral_constant<int, RG>{});
+    else tile_body(std::integral_constant<int, (RG > 1 ? RG - 1 : 1)>{});
   }
 
   __builtin_amdgcn_s_waitcnt(0);          // the ring's trailing DMAs land before exit
@@ -1441,10 +1458,10 @@ struct Plan {
   int max_splits;
 };
 
-// The three-row-group kernel as instantiated: 7 waves of 48 query rows (336
-// rows, one workgroup per CU with a four-tile ring), two 32-token softmax
-// steps per tile.
-constexpr int kRg3Waves = 7;
+// The three-row-group kernel as instantiated: 8 waves of up to 48 query rows
+// (one workgroup per CU, a two-tile ring), two 32-token softmax steps per
+// tile; planned for 257 - 384 rows.
+constexpr int kRg3Waves = 8;
 constexpr int kRg3Rows = kRg3Waves * 48;
 
 // MFMA workgroups one CU holds at once: bounded by LDS (the K/V ring plus the
@@ -1473,19 +1490,22 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   const int group = hq / hkv;
   const int rows = n_max * group;
   // Head dim 128: the 16-row kernel, in balanced row blocks of at most 256
-  // rows (8 waves up to 128 rows, else 16), except for 257 - 336 rows, which
-  // one workgroup of the three-row-group kernel covers (on the 80-node sweep
-  // tree it beats two 160-row blocks of the 16-row kernel, 115 vs 122 µs,
-  // which beat the 32-row kernel's 256 + 64 split, 153 µs). Head dim 64: the
-  // 16-row kernel up to 128 rows, else the 32-row kernel.
+  // rows (8 waves up to 128 rows, else 16), except for 257 - 384 rows, which
+  // one workgroup of the three-row-group kernel covers. Per call at 8k
+  // context x 8 sequences: 320 rows 126 µs against 144 for two 160-row
+  // blocks of the 16-row kernel, 352 rows 139 against 151; at 224 and 256
+  // rows the 16-row kernel's single block is ahead (103 vs 106, 109 vs 113).
+  // Head dim 64: the 16-row kernel up to 128 rows, else the 32-row kernel.
   p.rows48 = mfma && d == 128 && rows > 256 && rows <= kRg3Rows;
   p.rows16 = mfma && !p.rows48 && (d == 128 || rows <= 128);
   if (p.rows48) {
-    // 257 - 336 rows: one block of seven 48-row waves, so each K/V tile is
-    // streamed once per kv-head (two 16-row blocks would stream it twice)
-    // and every LDS operand read feeds three row groups.
+    // 257 - 384 rows: one block of eight waves of two or three 16-row groups,
+    // so each K/V tile is streamed once per kv-head (two 16-row blocks would
+    // stream it twice) and every LDS operand read feeds two or three row
+    // groups. The block holds exactly the launch's row groups, so the kernel
+    // deals them evenly over the SIMDs.
     p.row_blocks = 1;
-    p.rows_per_wg = kRg3Rows;
+    p.rows_per_wg = (rows + 15) / 16 * 16;
     p.nw = kRg3Waves;
   } else if (p.rows16) {
     // Row blocks of at most 256 rows, balanced, in multiples of 16.
@@ -1694,7 +1714,7 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
   // the same token range, so concurrent reads cover whole cache rows.
   const dim3 grid(hkv * p.row_blocks, p.max_splits, batch);
   if (p.rows48) {
-    hipLaunchKernelGGL((tree_attn_rg<128, kRg3Waves, 3, 4, 4, 2, 2>), grid, dim3(64 * kRg3Waves), 0,
+    hipLaunchKernelGGL((tree_attn_rg<128, kRg3Waves, 3, 2, 4, 2, 2>), grid, dim3(64 * kRg3Waves), 0,
                        st, a);
   } else if (p.rows16) {
     if (d == 128) {

@@ -235,17 +235,24 @@ def test_row_blocking_and_wide_trees(hq, hkv, d, n_ufp, depth):
         check_attn(w, o, lse, ref_o, ref_l)
 
 
-@pytest.mark.parametrize("n_ufp,depth,ctx,kv_split", [(12, 5, [300, 64], 0), (4, 17, [1000, 0], 0),
-                                                  (12, 5, [129, 2500], 3), (7, 7, [63, 700], 0),
-                                                  (12, 6, [2000, 65], 5)])
-def test_three_row_group_kernel(n_ufp, depth, ctx, kv_split):
-    # 257 - 336 rows per kv-head (group 4) take the kernel with three 16-row
-    # groups per wave: 76 nodes (304 rows), 84 (336, the block's capacity),
-    # 76 again with forced splits, 65 (260 rows, just past 256), and 88 nodes
-    # (352 rows: the 16-row kernel in two blocks) as a neighbour; the second
-    # tree is trimmed by 7 nodes so a wave's row groups end mid-node.
-    say("attn 48-row waves", n_ufp, depth, ctx, kv_split)
-    w = make_workload("r3", batch=2, hq=16, hkv=4, ctx_lens=ctx, chain_len=16, n_ufp=n_ufp,
+@pytest.mark.parametrize("hq,hkv,n_ufp,depth,ctx,kv_split", [
+    (16, 4, 12, 5, [300, 64], 0), (16, 4, 4, 17, [1000, 0], 0), (16, 4, 12, 5, [129, 2500], 3),
+    (16, 4, 7, 7, [63, 700], 0), (16, 4, 13, 4, [640, 97], 0), (16, 4, 14, 4, [65, 1300], 0),
+    (16, 4, 16, 4, [900, 200], 2), (32, 4, 6, 3, [500, 64], 0), (8, 4, 2, 67, [260, 31], 0),
+    (16, 4, 12, 6, [2000, 65], 5), (16, 4, 16, 5, [333, 1111], 0), (16, 4, 12, 7, [129, 64], 0)])
+def test_three_row_group_kernel(hq, hkv, n_ufp, depth, ctx, kv_split):
+    # 257 - 384 rows per kv-head take the kernel whose waves own two or three
+    # 16-row groups (waves with three come first). Group 4: 76 nodes (304
+    # rows, 19 row groups: three waves of three), 84 (336: five), 76 with
+    # forced splits, 65 (260 rows, just past 256: one), 68 (272: one), 72
+    # (288: two), 80 (320: four, every SIMD even) with forced splits, 88 (352:
+    # six) with forced splits, 96 (384, the block's capacity: all eight);
+    # group 8 at 34 nodes (272 rows) and group 2 at 150 nodes (300 rows); and
+    # 100 nodes (400 rows: the 16-row kernel in two blocks) as a neighbour.
+    # The second tree is trimmed by 7 nodes so a wave's row groups end
+    # mid-node and some waves own no rows.
+    say("attn 48-row waves", hq, hkv, n_ufp, depth, ctx, kv_split)
+    w = make_workload("r3", batch=2, hq=hq, hkv=hkv, ctx_lens=ctx, chain_len=16, n_ufp=n_ufp,
                       branch_depth=depth, seed=300 + n_ufp * 7 + depth)
     n_tree = int(w.n_nodes[0])
     _trim_trees(w, [n_tree, n_tree - 7])
