@@ -1,12 +1,14 @@
 """Benchmark: one CURE verify-and-repair step on one MI355X.
 
 A step is one pass of the whole hot path over one batch of synthetic input
-already resident in HBM:
-  1. cure_margins   over every tree node's logits row, with the UFP gate over
-                    the draft-chain rows (Sec. 3.3, Eq. 2, Algorithm 1),
-  2. cure_tree_attn one tree-masked verification attention layer (Sec. 3.5),
-  3. cure_accept    the acceptance walk, fed the margins' top-1 indices as the
-                    target argmax (Eq. 1, Eq. 4).
+already resident in HBM, in two calls:
+  1. cure_tree_attn one tree-masked verification attention layer (Sec. 3.5),
+  2. cure_margins_accept  the margin pass over every tree node's logits row,
+                    with the UFP gate over the draft-chain rows (Sec. 3.3,
+                    Eq. 2, Algorithm 1) and the acceptance walk on the rows'
+                    top-1 indices as the target argmax (Eq. 1, Eq. 4) -- the
+                    same outputs as cure_margins followed by cure_accept.
+The separate cure_margins and cure_accept calls are timed too (`kernels`).
 The repair-tree builder (cure_repair_tree: ranked alternatives at the UFPs,
 Eq. 3 branch budget, parent/token assembly) is timed beside the step, on the
 draft-chain rows and UFPs the step's margin pass produced; it is reported
@@ -57,9 +59,11 @@ ROTATE_BYTES = 512 << 20
 CSRC = os.path.join(ROOT, "paper_2608_00531_amd", "csrc")
 # Kernel sources behind each call: a stored traffic figure is used only while
 # these files are unchanged since the counters were taken.
-CALL_SOURCES = {"margins": ["margins.hip", "common.hpp"], "attn": ["tree_attn.hip", "common.hpp"],
-                "accept": ["accept.hip", "common.hpp"], "repair": ["repair.hip", "common.hpp"],
-                "commit": ["commit.hip", "common.hpp"]}
+CALL_SOURCES = {"margins": ["margins.hip", "common.hpp", "accept_walk.hpp"],
+                "margins_accept": ["margins.hip", "common.hpp", "accept_walk.hpp"],
+                "attn": ["tree_attn.hip", "common.hpp"],
+                "accept": ["accept.hip", "common.hpp", "accept_walk.hpp"],
+                "repair": ["repair.hip", "common.hpp"], "commit": ["commit.hip", "common.hpp"]}
 # Layers of the cache the commit runs over (a Llama-3-8B-class target).
 COMMIT_LAYERS = 32
 # Eq. 3 parameters of the repair-tree builder: the paper's b_min, b_max, and a
@@ -146,6 +150,12 @@ class Step:
             P(copy["parent"]), P(copy["token"]), P(self.m["top1_idx"]), P(copy["root_tgt"]),
             P(copy["n_nodes"]), w.chain_len, B, R, P(self.acc["acc_len"]), P(self.path),
             P(self.acc["best"]), P(self.acc["bonus"]), P(self.acc["resync"]), s)
+        # The margin pass with the acceptance walk as its epilogue: the step's
+        # margins and accept in the margin pass's two launches.
+        self.margins_accept_args = self.margins_args[:18] + (
+            P(copy["parent"]), P(copy["token"]), P(copy["root_tgt"]), P(copy["n_nodes"]),
+            P(self.acc["acc_len"]), P(self.path), P(self.acc["best"]), P(self.acc["bonus"]),
+            P(self.acc["resync"])) + self.margins_args[18:]
         self.repair_args = (
             P(copy["logits"]), pc.CURE_BF16 if w.dtype == "bf16" else pc.CURE_F32, B, R, V, V,
             P(self.m["margin"]), P(self.ufp_pos), P(self.ufp_cnt), P(copy["chain_tok"]), K,
@@ -181,6 +191,11 @@ class Step:
         if st:
             raise RuntimeError("cure_accept status %d" % st)
 
+    def margins_accept(self):
+        st = self.L.cure_margins_accept(*self.margins_accept_args)
+        if st:
+            raise RuntimeError("cure_margins_accept status %d" % st)
+
     def repair(self):
         st = self.L.cure_repair_tree(*self.repair_args)
         if st:
@@ -192,9 +207,11 @@ class Step:
             raise RuntimeError("cure_commit status %d" % st)
 
     def run(self):
-        self.margins()
+        """One step, in the method's order: the tree-masked verification
+        attention with its merge, then the margin pass over the nodes' logits
+        with its UFP gate and the acceptance walk on their argmaxes."""
         self.attn()
-        self.accept()
+        self.margins_accept()
 
 
 def upload_copy(torch, w):
@@ -389,7 +406,7 @@ def kernel_times(torch, steps, call, k):
     return out
 
 
-CALLS = ("margins", "attn", "accept", "repair", "commit")
+CALLS = ("margins", "attn", "accept", "margins_accept", "repair", "commit")
 
 
 def per_call_samples(torch, steps, k, calls=CALLS, warmup=0):
@@ -583,7 +600,7 @@ def measure(w, args, torch, pc):
             assert torch.equal(st.o, o)
         k_calls = min(args.steps, 100)
         call_samples = per_call_samples(torch, steps, k_calls)
-        kern = {c: kernel_times(torch, steps, c, k_calls) for c in ("margins", "attn", "accept")}
+        kern = {c: kernel_times(torch, steps, c, k_calls) for c in ("margins_accept", "attn")}
     calls = {c: float(np.mean(v)) for c, v in call_samples.items()}
     status = steps[0].status.cpu().tolist()
     assert status == [0] * w.batch, status
@@ -593,6 +610,7 @@ def measure(w, args, torch, pc):
     assert steps[0].com["status"].cpu().tolist() == [0] * w.batch
 
     call_bytes = {"margins": ab["margins"], "attn": ab["attention"], "accept": ab["accept"],
+                  "margins_accept": ab["margins"] + ab["accept"],
                   "repair": rep_bytes, "commit": com_bytes}
     kernels = {}
     for name, us in calls.items():

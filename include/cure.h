@@ -10,6 +10,8 @@
  *   cure_tree_attn  tree-masked verification attention over the KV cache and
  *                   each node's own tree ancestors           (Sec. 3.2, 3.4, 3.5)
  *   cure_accept     accepted prefix per path and the best path     (Eq. 1, Eq. 4)
+ *   cure_margins_accept  cure_margins over a tree's node logits followed by
+ *                   cure_accept on their argmaxes, in the margin pass's launches
  *   cure_repair_tree  the budget-aware repair tree: ranked alternatives at the
  *                   UFPs, the Eq. 3 branch budget and the parent/token arrays
  *                                                       (Sec. 3.3, 3.4, Alg. 1)
@@ -110,6 +112,35 @@ cure_status cure_margins(const void* logits, int32_t dtype, int32_t batch, int32
                          int32_t chain_len, float tau, int32_t repair_budget,
                          int32_t branch_depth, int32_t* ufp_pos, int32_t* ufp_cnt,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Margin pass with the acceptance walk as its epilogue -- Sec. 3.3 Eq. (2),
+ * Algorithm 1, Sec. 3.1 Eq. (1), Sec. 3.5 Eq. (4).
+ *
+ * For logits whose rows are the nodes of each sequence's candidate tree (row
+ * n of sequence b = node n, so rows is the tree arrays' n_max): exactly
+ * cure_margins(...) followed by cure_accept(parent, token, top1_idx, root_tgt,
+ * n_nodes, chain_len, batch, rows, ...), with every output of both, bit for
+ * bit. The walk runs in the workgroup that finishes each sequence's rows, so
+ * the pair costs the margin pass's launches only (no separate acceptance
+ * launch). chain_len serves the UFP gate (when ufp_pos/ufp_cnt are given) and
+ * the walk's resync flag.
+ *   parent, token  [batch][rows] int32;  root_tgt, n_nodes  [batch] int32
+ *   acc_len, best, bonus, resync  [batch] int32;  path  [batch][rows] int32
+ * Requires everything cure_margins requires, chain_len >= 0 and rows <= 256
+ * (CURE_ERR_UNSUPPORTED otherwise). workspace: cure_margins_workspace_size(
+ * batch, rows, vocab) bytes.
+ */
+cure_status cure_margins_accept(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
+                                int32_t vocab, int64_t ld,
+                                float* top1_val, int32_t* top1_idx, float* top2_val,
+                                int32_t* top2_idx, float* lse, float* margin,
+                                int32_t chain_len, float tau, int32_t repair_budget,
+                                int32_t branch_depth, int32_t* ufp_pos, int32_t* ufp_cnt,
+                                const int32_t* parent, const int32_t* token,
+                                const int32_t* root_tgt, const int32_t* n_nodes,
+                                int32_t* acc_len, int32_t* path, int32_t* best,
+                                int32_t* bonus, int32_t* resync,
+                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* Allocation-free margin pass, for callers that cannot allocate device memory
  * (code under HIP stream capture, tight serving loops, harnesses that forbid

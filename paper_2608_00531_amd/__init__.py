@@ -5,7 +5,7 @@ thin ctypes binding (names match the C entry points).
 """
 
 from .cure import (  # noqa: F401
-    cure_margins, cure_margins_noalloc, cure_tree_attn, cure_tree_attn_workspace_size, cure_accept,
+    cure_margins, cure_margins_accept, cure_margins_noalloc, cure_tree_attn, cure_tree_attn_workspace_size, cure_accept,
     cure_repair_tree, cure_commit, cure_read_ceiling, lib,
     library_path, CureError, CURE_OK, CURE_ERR_INVALID_ARG, CURE_ERR_UNSUPPORTED,
     CURE_ERR_BAD_TREE, CURE_ERR_HIP, CURE_ERR_WORKSPACE, CURE_F32, CURE_BF16,

@@ -15,7 +15,8 @@
 // With one chunk per row the workgroup writes the row's results itself. With
 // several, chunk results go to the workspace and margins_finish (one workgroup
 // per sequence) merges them with an associative (value desc, index asc) top-2
-// merge; the same kernel runs the UFP selection. Workgroups never wait on each
+// merge; the same kernel runs the UFP selection and, for cure_margins_accept,
+// the acceptance walk over the rows' argmaxes (Eq. 1, Eq. 4). Workgroups never wait on each
 // other inside a kernel: on a multi-die GPU the device-scope fences such a
 // hand-off needs cost far more than a second, tiny launch.
 #include <hip/hip_runtime.h>
@@ -23,6 +24,7 @@
 #include <algorithm>
 #include <mutex>
 
+#include "accept_walk.hpp"
 #include "common.hpp"
 #include "host_util.hpp"
 
@@ -59,6 +61,14 @@ struct Args {
   int32_t* ufp_pos;
   int32_t* ufp_cnt;
   Partial* partials;     // [rows total][splits], only when splits > 1
+  // Acceptance epilogue (cure_margins_accept; acc.acc_len == nullptr: none).
+  // The rows of a sequence are its tree's nodes, row n = node n.
+  const int32_t* parent;
+  const int32_t* token;
+  const int32_t* root_tgt;
+  const int32_t* n_nodes;
+  int32_t acc_chain;
+  AcceptOut acc;
 };
 
 // Raw buffer loads: the chunk is described by a buffer resource (base, size)
@@ -161,6 +171,25 @@ CURE_DEV void select_ufp(const Args& a, int b, const float* sm) {
   const int cnt = min(s_cnt, a.max_ufp);
   for (int p = cnt + threadIdx.x; p < K; p += kThreads) a.ufp_pos[(int64_t)b * K + p] = -1;
   if (threadIdx.x == 0) a.ufp_cnt[b] = cnt;
+}
+
+// The same selection by one wave, for chain_len <= 64: lane i ranks position i
+// and the candidates are counted with a ballot, so no barrier is needed.
+CURE_DEV void select_ufp_wave(const Args& a, int b, const float* sm) {
+  const int K = a.chain_len;
+  const int i = threadIdx.x % kWave;
+  const float mi = i < K ? sm[i] : 0.f;
+  const bool cand = i < K && mi < a.tau;
+  int rank = 0;
+  if (cand)
+    for (int j = 0; j < K; ++j) {
+      const float mj = sm[j];
+      rank += (mj < a.tau) && (mj < mi || (mj == mi && j < i));
+    }
+  const int cnt = min((int)__popcll(__ballot(cand)), a.max_ufp);
+  if (cand && rank < a.max_ufp) a.ufp_pos[(int64_t)b * K + rank] = i;
+  for (int q = cnt + i; q < K; q += kWave) a.ufp_pos[(int64_t)b * K + q] = -1;
+  if (i == 0) a.ufp_cnt[b] = cnt;
 }
 
 template <typename T, bool kVecPath>
@@ -339,7 +368,27 @@ static_assert(kMaxSplits % kFinishGroup == 0, "chunk results split evenly over a
 
 __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
   __shared__ float s_margin[kMaxGateChain];
+  __shared__ AcceptLds<kThreads> s_acc;
   const int b = blockIdx.x;
+  const bool accept = a.acc.acc_len != nullptr;
+  // Chains of up to 64 rows (and trees of up to 64 nodes): after the merge,
+  // wave 0 runs the gate and wave 1 the acceptance walk, side by side and
+  // without barriers.
+  const bool by_waves = a.chain_len <= kWave && (!accept || a.rows <= kWave);
+  const int wave = threadIdx.x / kWave;
+  // The tree's arrays are loaded before the chunk results are merged, by the
+  // thread standing for each node.
+  const int node = by_waves ? (int)threadIdx.x - kWave : (int)threadIdx.x;
+  int p = -1, tok = 0, nn = 0, root = 0;
+  if (accept) {
+    const int64_t row = (int64_t)b * a.rows;
+    nn = a.n_nodes[b];
+    root = a.root_tgt[b];
+    if (node >= 0 && node < a.rows) {
+      p = a.parent[row + node];
+      tok = a.token[row + node];
+    }
+  }
   if (a.splits > 1) {
     constexpr int kRowsPerPass = kThreads / kFinishGroup;
     const int k = threadIdx.x % kFinishGroup;
@@ -372,16 +421,30 @@ __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
       if (live && k == 0) {
         write_row(a, b * a.rows + r, t, lse_value(ls));
         if (r < a.chain_len) s_margin[r] = t.v1 - t.v2;
+        if (accept) s_acc.tgt[r] = t.i1;
       }
     }
-  } else if (a.ufp_pos) {
-    for (int i = threadIdx.x; i < a.chain_len; i += kThreads)
-      s_margin[i] = a.margin[(int64_t)b * a.rows + i];
+  } else {
+    if (a.ufp_pos)
+      for (int i = threadIdx.x; i < a.chain_len; i += kThreads)
+        s_margin[i] = a.margin[(int64_t)b * a.rows + i];
+    if (accept)
+      for (int i = threadIdx.x; i < a.rows; i += kThreads)
+        s_acc.tgt[i] = a.top1_idx[(int64_t)b * a.rows + i];
+  }
+  if (by_waves) {
+    __syncthreads();                     // the margins and argmaxes are in LDS
+    if (wave == 0 && a.ufp_pos) select_ufp_wave(a, b, s_margin);
+    if (wave == 1 && accept)
+      accept_walk<kWave, true>(s_acc, node, b, p, tok, nn, root, a.rows, a.acc_chain, a.acc);
+    return;
   }
   if (a.ufp_pos) {
     __syncthreads();
     select_ufp(a, b, s_margin);
   }
+  if (accept)
+    accept_walk<kThreads, false>(s_acc, node, b, p, tok, nn, root, a.rows, a.acc_chain, a.acc);
 }
 
 // Scratch of the allocation-free entry point: the chunk results of one call
@@ -432,14 +495,24 @@ cure_status check_args(const void* logits, int32_t dtype, int32_t batch, int32_t
   return CURE_OK;
 }
 
+// The acceptance walk's inputs and outputs (cure_margins_accept).
+struct AcceptIn {
+  const int32_t* parent;
+  const int32_t* token;
+  const int32_t* root_tgt;
+  const int32_t* n_nodes;
+  AcceptOut out;
+};
+
 // Launches the pass; `partials` holds the plan's chunk results (nrow * splits
-// records) when rows are split. The arguments have passed check_args.
+// records) when rows are split; `acc` (or nullptr) adds the acceptance walk.
+// The arguments have passed check_args.
 cure_status launch(const void* logits, int32_t dtype, int32_t batch, int32_t rows,
                    int32_t vocab, int64_t ld, float* top1_val, int32_t* top1_idx,
                    float* top2_val, int32_t* top2_idx, float* lse, float* margin,
                    int32_t chain_len, float tau, int32_t repair_budget, int32_t branch_depth,
                    int32_t* ufp_pos, int32_t* ufp_cnt, const Plan& pl, void* partials,
-                   void* stream) {
+                   const AcceptIn* acc, void* stream) {
   const bool gate = ufp_pos != nullptr;
   const int64_t nrow = (int64_t)batch * rows;
   const size_t esize = dtype == CURE_F32 ? 4 : 2;
@@ -467,6 +540,12 @@ cure_status launch(const void* logits, int32_t dtype, int32_t batch, int32_t row
   a.ufp_pos = gate ? ufp_pos : nullptr;
   a.ufp_cnt = gate ? ufp_cnt : nullptr;
   a.partials = reinterpret_cast<Partial*>(partials);
+  a.parent = acc ? acc->parent : nullptr;
+  a.token = acc ? acc->token : nullptr;
+  a.root_tgt = acc ? acc->root_tgt : nullptr;
+  a.n_nodes = acc ? acc->n_nodes : nullptr;
+  a.acc_chain = chain_len;
+  a.acc = acc ? acc->out : AcceptOut{nullptr, nullptr, nullptr, nullptr, nullptr};
 
   const dim3 grid((unsigned)(nrow * pl.splits)), block(kThreads);
   hipStream_t s = as_stream(stream);
@@ -478,7 +557,7 @@ cure_status launch(const void* logits, int32_t dtype, int32_t batch, int32_t row
     else hipLaunchKernelGGL((margins_kernel<float, false>), grid, block, 0, s, a);
   }
   if (hipGetLastError() != hipSuccess) return CURE_ERR_HIP;
-  if (pl.splits > 1 || gate)
+  if (pl.splits > 1 || gate || acc)
     hipLaunchKernelGGL(margins_finish, dim3(batch), block, 0, s, a);
   return launch_status();
 }
@@ -527,7 +606,40 @@ extern "C" cure_status cure_margins(const void* logits, int32_t dtype, int32_t b
     return CURE_ERR_WORKSPACE;
   return launch(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx, top2_val, top2_idx,
                 lse, margin, chain_len, tau, repair_budget, branch_depth, ufp_pos, ufp_cnt, pl,
-                workspace, stream);
+                workspace, nullptr, stream);
+}
+
+extern "C" cure_status cure_margins_accept(
+    const void* logits, int32_t dtype, int32_t batch, int32_t rows, int32_t vocab, int64_t ld,
+    float* top1_val, int32_t* top1_idx, float* top2_val, int32_t* top2_idx, float* lse,
+    float* margin, int32_t chain_len, float tau, int32_t repair_budget, int32_t branch_depth,
+    int32_t* ufp_pos, int32_t* ufp_cnt, const int32_t* parent, const int32_t* token,
+    const int32_t* root_tgt, const int32_t* n_nodes, int32_t* acc_len, int32_t* path,
+    int32_t* best, int32_t* bonus, int32_t* resync, void* workspace, size_t workspace_bytes,
+    void* stream) {
+  const cure_status st = check_args(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx,
+                                    top2_val, top2_idx, lse, margin, chain_len, repair_budget,
+                                    branch_depth, ufp_pos, ufp_cnt);
+  if (st != CURE_OK || batch == 0) return st;
+  if (chain_len < 0) return CURE_ERR_INVALID_ARG;
+  if (!parent || !token || !root_tgt || !n_nodes || !acc_len || !best || !bonus || !resync ||
+      (rows > 0 && !path))
+    return CURE_ERR_INVALID_ARG;
+  if (rows > CURE_MAX_TREE_NODES) return CURE_ERR_UNSUPPORTED;
+  if (rows == 0) {
+    // No nodes and no rows: nothing is accepted (the walk alone, on empty trees).
+    return cure_accept(parent, token, top1_idx, root_tgt, n_nodes, chain_len, batch, 0,
+                       acc_len, path, best, bonus, resync, stream);
+  }
+  const Plan pl = make_plan((int64_t)batch * rows, vocab);
+  if (pl.splits > 1 &&
+      (!workspace || workspace_bytes < cure_margins_workspace_size(batch, rows, vocab)))
+    return CURE_ERR_WORKSPACE;
+  const AcceptIn acc{parent, token, root_tgt, n_nodes,
+                     AcceptOut{acc_len, path, best, bonus, resync}};
+  return launch(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx, top2_val, top2_idx,
+                lse, margin, chain_len, tau, repair_budget, branch_depth, ufp_pos, ufp_cnt, pl,
+                workspace, &acc, stream);
 }
 
 extern "C" size_t cure_margins_noalloc_scratch_bytes(void) { return kScratchBytes; }
@@ -553,5 +665,5 @@ extern "C" cure_status cure_margins_noalloc(const void* logits, int32_t dtype, i
   }
   return launch(logits, dtype, batch, rows, vocab, ld, top1_val, top1_idx, top2_val, top2_idx,
                 lse, margin, chain_len, tau, repair_budget, branch_depth, ufp_pos, ufp_cnt, pl,
-                ws, stream);
+                ws, nullptr, stream);
 }

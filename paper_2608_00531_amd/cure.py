@@ -40,6 +40,11 @@ _SIGNATURES = {
     "cure_margins": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64,
                                     _vp, _vp, _vp, _vp, _vp, _vp,
                                     _i32, _f32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
+    "cure_margins_accept": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64,
+                                           _vp, _vp, _vp, _vp, _vp, _vp,
+                                           _i32, _f32, _i32, _i32, _vp, _vp,
+                                           _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                           _vp, _sz, _vp]),
     "cure_margins_noalloc_scratch_bytes": (_sz, []),
     "cure_margins_noalloc": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _i64,
                                             _vp, _vp, _vp, _vp, _vp, _vp,
@@ -162,6 +167,48 @@ def cure_margins(logits, chain_len=0, tau=float("inf"), repair_budget=0, branch_
                         chain_len, tau, repair_budget, branch_depth, _ptr(ufp_pos),
                         _ptr(ufp_cnt), _ptr(ws), wsb, _stream(dev))
     _check(st, "cure_margins")
+    return out
+
+
+def cure_margins_accept(logits, parent, token, root_tgt, n_nodes, chain_len, tau=float("inf"),
+                        repair_budget=0, branch_depth=1, gate=True):
+    """Margin pass over a tree's node logits [batch, n_max, vocab] followed by
+    the acceptance walk on their argmaxes, in one call. parent/token int32
+    [batch, n_max], root_tgt/n_nodes int32 [batch] (GPU tensors). Returns
+    cure_margins' dict plus cure_accept's (acc_len, path, best, bonus, resync)."""
+    _require_cuda(logits, parent, token, root_tgt, n_nodes)
+    x = logits if logits.dim() == 3 else logits.unsqueeze(0)
+    if x.stride(2) != 1 or x.stride(0) != x.shape[1] * x.stride(1):
+        x = x.contiguous()
+    batch, rows, vocab = x.shape
+    dev = x.device
+    f = dict(dtype=torch.float32, device=dev)
+    i = dict(dtype=torch.int32, device=dev)
+    out = {
+        "top1_val": torch.empty(batch, rows, **f), "top1_idx": torch.empty(batch, rows, **i),
+        "top2_val": torch.empty(batch, rows, **f), "top2_idx": torch.empty(batch, rows, **i),
+        "lse": torch.empty(batch, rows, **f), "margin": torch.empty(batch, rows, **f),
+        "acc_len": torch.empty(batch, **i), "path": torch.empty(batch, rows, **i),
+        "best": torch.empty(batch, **i), "bonus": torch.empty(batch, **i),
+        "resync": torch.empty(batch, **i),
+    }
+    ufp_pos = ufp_cnt = None
+    if gate:
+        ufp_pos = torch.empty(batch, chain_len, **i)
+        ufp_cnt = torch.empty(batch, **i)
+        out["ufp_pos"], out["ufp_cnt"] = ufp_pos, ufp_cnt
+    tree = [t.contiguous() for t in (parent, token, root_tgt, n_nodes)]
+    L = lib()
+    ws, wsb = _workspace("margins", dev, L.cure_margins_workspace_size(batch, rows, vocab))
+    st = L.cure_margins_accept(_ptr(x), _dtype_code(x), batch, rows, vocab, x.stride(1),
+                               _ptr(out["top1_val"]), _ptr(out["top1_idx"]),
+                               _ptr(out["top2_val"]), _ptr(out["top2_idx"]), _ptr(out["lse"]),
+                               _ptr(out["margin"]), chain_len, tau, repair_budget, branch_depth,
+                               _ptr(ufp_pos), _ptr(ufp_cnt), *[_ptr(t) for t in tree],
+                               _ptr(out["acc_len"]), _ptr(out["path"]), _ptr(out["best"]),
+                               _ptr(out["bonus"]), _ptr(out["resync"]), _ptr(ws), wsb,
+                               _stream(dev))
+    _check(st, "cure_margins_accept")
     return out
 
 

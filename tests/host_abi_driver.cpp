@@ -63,6 +63,20 @@ int main() {
   expect(margins_na(1, 1 << 20, 4096, 128256, 128256, P, 2, 4, I, I), CURE_ERR_UNSUPPORTED,
          "noalloc too many rows");
   expect(cure_margins_noalloc_scratch_bytes() == 256 * 1024, 1, "noalloc scratch size");
+
+  // Margin pass with the acceptance walk: its own checks after cure_margins'.
+  auto margins_acc = [&](int batch, int rows, int vocab, int chain, const int32_t* parent,
+                         int32_t* path) {
+    return (int)cure_margins_accept(P, 1, batch, rows, vocab, vocab, F, I, F, I, F, F, chain,
+                                    1.0f, 4, 2, nullptr, nullptr, parent, I, I, I, I, path, I,
+                                    I, I, nullptr, 0, nullptr);
+  };
+  expect(margins_acc(1, 4, 1000, 2, nullptr, I), CURE_ERR_INVALID_ARG, "margins_accept parent");
+  expect(margins_acc(1, 4, 1000, 2, I, nullptr), CURE_ERR_INVALID_ARG, "margins_accept path");
+  expect(margins_acc(1, 4, 1000, -1, I, I), CURE_ERR_INVALID_ARG, "margins_accept chain");
+  expect(margins_acc(1, 300, 1000, 2, I, I), CURE_ERR_UNSUPPORTED, "margins_accept rows");
+  expect(margins_acc(1, 4, 100000, 2, I, I), CURE_ERR_WORKSPACE, "margins_accept workspace");
+  expect(margins_acc(0, 4, 100000, 2, I, I), CURE_OK, "margins_accept empty");
   size_t last = 0;
   for (int b : {1, 7, 16, 1024})
     for (int r : {1, 32, 48, 333})

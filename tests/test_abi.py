@@ -77,6 +77,32 @@ def test_margins_argument_errors(L):
     assert _margins(L, batch=-1) == pc.CURE_ERR_INVALID_ARG
 
 
+def test_margins_accept_argument_errors(L):
+    # cure_margins' host checks, then the acceptance walk's, before any device
+    # is touched (vocab 100000 over 4 rows splits the rows, so a missing
+    # workspace is reported rather than a launch).
+    def call(**kw):
+        args = dict(logits=1, dtype=1, batch=1, rows=4, vocab=100000, ld=100000,
+                    top1_val=1, top1_idx=1, top2_val=1, top2_idx=1, lse=1, margin=1,
+                    chain_len=2, tau=1.0, repair_budget=4, branch_depth=2, ufp_pos=1,
+                    ufp_cnt=1, parent=1, token=1, root_tgt=1, n_nodes=1, acc_len=1, path=1,
+                    best=1, bonus=1, resync=1, workspace=None, ws_bytes=0, stream=None)
+        args.update(kw)
+        return L.cure_margins_accept(*args.values())
+    assert call(dtype=7) == pc.CURE_ERR_INVALID_ARG
+    assert call(logits=None) == pc.CURE_ERR_INVALID_ARG
+    assert call(ufp_cnt=None) == pc.CURE_ERR_INVALID_ARG              # half a gate
+    assert call(chain_len=5) == pc.CURE_ERR_INVALID_ARG               # > rows with the gate
+    assert call(ufp_pos=None, ufp_cnt=None, chain_len=-1) == pc.CURE_ERR_INVALID_ARG
+    for k in ("parent", "token", "root_tgt", "n_nodes", "acc_len", "path", "best", "bonus",
+              "resync"):
+        assert call(**{k: None}) == pc.CURE_ERR_INVALID_ARG, k
+    assert call(rows=257) == pc.CURE_ERR_UNSUPPORTED                    # not a tree's nodes
+    assert call() == pc.CURE_ERR_WORKSPACE                              # no workspace
+    assert call(batch=0) == pc.CURE_OK
+    assert call(batch=-1) == pc.CURE_ERR_INVALID_ARG
+
+
 def test_margins_noalloc_argument_errors(L):
     # The same host checks as cure_margins, before any device is touched.
     def call(**kw):
