@@ -1,8 +1,8 @@
-"""GPU: the whole verify-and-repair step (margins -> tree attention -> accept)
-on named workloads, chained exactly as the benchmark chains it, checked against
-the oracle chained the same way; and the step captured as a HIP graph,
-replayed several times with eager work in between, each replay checked
-against the eager result.
+"""GPU: the whole verify-and-repair step (tree attention, margins with the UFP
+gate, accept) on named workloads, both as three calls and as the benchmark's
+two (cure_tree_attn, cure_margins_accept), checked against the oracle chained
+the same way; and the step captured as a HIP graph, replayed several times
+with eager work in between, each replay checked against the eager result.
 """
 
 import numpy as np
@@ -18,22 +18,29 @@ from parity_util import (say, upload, gpu_margins, gpu_attn, check_margins, chec
 pytestmark = pytest.mark.gpu
 
 
-def run_step(w, dev):
-    m = gpu_margins(w, dev)
+def run_step(w, dev, fused=False):
     o, lse, st = gpu_attn(w, dev)
-    acc = pc.cure_accept(dev["parent"], dev["token"], m["top1_idx"], dev["root_tgt"],
-                         dev["n_nodes"], w.chain_len)
+    if fused:
+        m = pc.cure_margins_accept(dev["logits"], dev["parent"], dev["token"], dev["root_tgt"],
+                                   dev["n_nodes"], w.chain_len, tau=w.tau,
+                                   repair_budget=w.repair_budget, branch_depth=w.branch_depth)
+        acc = m
+    else:
+        m = gpu_margins(w, dev)
+        acc = pc.cure_accept(dev["parent"], dev["token"], m["top1_idx"], dev["root_tgt"],
+                             dev["n_nodes"], w.chain_len)
     return m, (o, lse, st), acc
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", ["tiny_fp32", "llama3_8b_ctx2k_b1",
                                   "llama3_8b_ctx8k_b8_budget32", "llama3_8b_ragged_b16",
                                   "llama3_8b_ctx8k_b8_budget64"])
-def test_step_chain_matches_oracle_chain(name):
-    say("step", name)
+def test_step_chain_matches_oracle_chain(name, fused):
+    say("step", name, "fused" if fused else "three calls")
     w = preset(name)
     dev = upload(w)
-    m, (o, lse, st), acc = run_step(w, dev)
+    m, (o, lse, st), acc = run_step(w, dev, fused)
     torch.cuda.synchronize()
     assert st.tolist() == [pc.CURE_OK] * w.batch
     check_margins(w, m)
@@ -45,17 +52,18 @@ def test_step_chain_matches_oracle_chain(name):
     check_attn(w, o, lse, ref_o, ref_l, sample=sample)
 
 
-def test_graph_replays_match_eager():
-    say("step graph replay")
+@pytest.mark.parametrize("fused", [False, True])
+def test_graph_replays_match_eager(fused):
+    say("step graph replay", "fused" if fused else "three calls")
     w = preset("llama3_8b_ctx2k_b1")
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
         dev = upload(w)
-        eager = run_step(w, dev)
+        eager = run_step(w, dev, fused)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=s):
-            cap = run_step(w, dev)
+            cap = run_step(w, dev, fused)
         for rep in range(4):
             # Eager work and a synchronisation between replays.
             junk = torch.randn(1 << 20, device="cuda").sum()
@@ -85,7 +93,7 @@ def test_graph_replays_ragged_batch_with_repair():
         chain_tok = dev["token"][:, : w.chain_len].contiguous()
 
         def step():
-            m, att, acc = run_step(w, dev)
+            m, att, acc = run_step(w, dev, fused=True)
             rep = pc.cure_repair_tree(dev["logits"], m["margin"], m["ufp_pos"], m["ufp_cnt"],
                                       chain_tok, w.repair_budget, w.branch_depth, w.tau)
             return m, att, acc, rep
