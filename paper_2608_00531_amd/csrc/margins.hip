@@ -379,13 +379,13 @@ __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
   // The tree's arrays are loaded before the chunk results are merged, by the
   // thread standing for each node.
   const int node = by_waves ? (int)threadIdx.x - kWave : (int)threadIdx.x;
-  int p = -1, tok = 0, nn = 0, root = 0;
+  int par = -1, tok = 0, nn = 0, root = 0;
   if (accept) {
     const int64_t row = (int64_t)b * a.rows;
     nn = a.n_nodes[b];
     root = a.root_tgt[b];
     if (node >= 0 && node < a.rows) {
-      p = a.parent[row + node];
+      par = a.parent[row + node];
       tok = a.token[row + node];
     }
   }
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
     __syncthreads();                     // the margins and argmaxes are in LDS
     if (wave == 0 && a.ufp_pos) select_ufp_wave(a, b, s_margin);
     if (wave == 1 && accept)
-      accept_walk<kWave, true>(s_acc, node, b, p, tok, nn, root, a.rows, a.acc_chain, a.acc);
+      accept_walk<kWave, true>(s_acc, node, b, par, tok, nn, root, a.rows, a.acc_chain, a.acc);
     return;
   }
   if (a.ufp_pos) {
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(kThreads) void margins_finish(Args a) {
     select_ufp(a, b, s_margin);
   }
   if (accept)
-    accept_walk<kThreads, false>(s_acc, node, b, p, tok, nn, root, a.rows, a.acc_chain, a.acc);
+    accept_walk<kThreads, false>(s_acc, node, b, par, tok, nn, root, a.rows, a.acc_chain, a.acc);
 }
 
 // Scratch of the allocation-free entry point: the chunk results of one call
