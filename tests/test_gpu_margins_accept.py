@@ -129,3 +129,35 @@ def test_empty_trees_and_argument_errors():
                                P(dummy), P(dummy), P(root), P(nn), P(outs[0]), P(dummy),
                                P(outs[1]), P(outs[2]), P(outs[3]), P(dummy), 1 << 20, None)
     assert st == pc.CURE_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("vocab,dtype", [(3001, torch.float32), (40000, torch.bfloat16)])
+def test_padded_rows_and_ties(vocab, dtype):
+    # Rows padded by 3 entries (ld = vocab + 3: the margin pass's scalar path),
+    # rows split (40000) or not (3001), and every row's maximum repeated so the
+    # argmax the walk uses is decided by the lowest-index rule.
+    say("margins+accept padded", vocab, dtype)
+    rng = np.random.default_rng(vocab)
+    B, n_max = 3, 40
+    big = torch.from_numpy(rng.standard_normal((B, n_max, vocab + 3)).astype(np.float32))
+    cols = rng.integers(0, vocab, (B, n_max, 2))
+    for b in range(B):
+        for n in range(n_max):
+            big[b, n, cols[b, n]] = 9.0
+    x = big.to(dtype).cuda()[:, :, :vocab]
+    assert x.stride(1) == vocab + 3
+    parent = np.full((B, n_max), -1, np.int32)
+    for b in range(B):
+        for n in range(1, n_max):
+            parent[b, n] = n - 1 if n < 20 else int(rng.integers(10, n))
+    # Tokens equal to the argmax the target will produce, so the chain is accepted.
+    am = np.minimum(cols[:, :, 0], cols[:, :, 1]).astype(np.int32)
+    token = np.zeros((B, n_max), np.int32)
+    root = am[:, 0].copy()
+    for b in range(B):
+        token[b, 0] = root[b]
+        for n in range(1, n_max):
+            token[b, n] = am[b, parent[b, n]]
+    out = _check(x, parent, token, root, np.full(B, n_max, np.int32), 16, 0.5, 8, 2, True)
+    assert out["top1_idx"].cpu().numpy().tolist() == am.tolist()
+    assert int(out["acc_len"].min()) >= 20
