@@ -122,7 +122,20 @@ struct Raw8<float> {
 // excludes NaN logits), so no quieting of the operands is needed.
 CURE_DEV float max3(float a, float b, float c) {
   float r;
-  asm volatile("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Two-input maximum and minimum on the VALU, without the operand quieting
+// fmaxf/fminf add for values of unknown origin (the inputs are never NaN).
+CURE_DEV float max_raw(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+CURE_DEV float min_raw(float a, float b) {
+  float r;
+  asm("v_min_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
 }
 
@@ -247,9 +260,9 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
           const bool c2 = ok && m8[u] > bm2;
           bv2 = c1 ? bv1 : (c2 ? v : bv2);
           bv1 = c1 ? v : bv1;
-          bm2 = fmaxf(bm2, fminf(m8[u], bm1));
-          bm1 = fmaxf(bm1, m8[u]);
-          step_max = fmaxf(step_max, m8[u]);
+          bm2 = max_raw(bm2, min_raw(m8[u], bm1));
+          bm1 = max_raw(bm1, m8[u]);
+          step_max = max_raw(step_max, m8[u]);
         }
         // Log-sum-exp against a lagging reference, moved only on large jumps
         // (checked once per step, before the step's terms are added).
@@ -265,9 +278,12 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
         for (int u = 0; u < kUnroll; ++u) {
           const int v = (it * kUnroll + u) * kThreads + tid;
           if (!checked || v < nvec) {
-            float s0 = 0.f, s1 = 0.f;
+            // Exponentials are never negative, so starting each partial sum at
+            // its first term gives the same bits as starting at zero.
+            float s0 = fast_exp2(fmaf(f[u][0], kLog2e, nref));
+            float s1 = fast_exp2(fmaf(f[u][1], kLog2e, nref));
 #pragma unroll
-            for (int j = 0; j < kVec; j += 2) {
+            for (int j = 2; j < kVec; j += 2) {
               s0 += fast_exp2(fmaf(f[u][j], kLog2e, nref));
               s1 += fast_exp2(fmaf(f[u][j + 1], kLog2e, nref));
             }
