@@ -1177,32 +1177,32 @@ void tree_attn_rg(Args a) {
     // The tile's work for NG row groups (NG = RG or RG - 1, this wave's count).
     auto tile_body = [&](auto ng) {
       constexpr int NG = decltype(ng)::value;
-  #pragma unroll
+#pragma unroll
       for (int hs = 0; hs < HT; ++hs) {
         // Scores of this step's kTB 16-token blocks x NG row groups, each a
         // chain of kKSteps MFMAs; every K fragment feeds all NG groups.
         f32x4 sacc[NG][kTB];
-  #pragma unroll
+#pragma unroll
         for (int rg = 0; rg < NG; ++rg)
-  #pragma unroll
+#pragma unroll
           for (int tb = 0; tb < kTB; ++tb) sacc[rg][tb] = f32x4{0.f, 0.f, 0.f, 0.f};
         Pack8 kf[kKFrags];
         auto load_k = [&](Pack8& f, int i) {
           f.u = *reinterpret_cast<const uint4*>(kt + (hs * kTB + i % kTB) * 16 * G::kRowBytes +
                                                 k_off[i / kTB]);
         };
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < kAheadK; ++i) load_k(kf[i], i);
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < kKFrags; ++i) {
           if (i + kAheadK < kKFrags) load_k(kf[i + kAheadK], i + kAheadK);
-  #pragma unroll
+#pragma unroll
           for (int rg = 0; rg < NG; ++rg)
             sacc[rg][i % kTB] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[i].v, qreg[rg][i / kTB],
                                                                        sacc[rg][i % kTB], 0, 0, 0);
         }
         __builtin_amdgcn_sched_group_barrier(0x100, kAheadK, 0);
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < kKFrags - kAheadK; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, NG, 0);
           __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
@@ -1210,11 +1210,11 @@ void tree_attn_rg(Args a) {
         __builtin_amdgcn_sched_group_barrier(0x008, NG * kAheadK, 0);
         const int s0 = t0 + hs * 16 * kTB;             // first token of this step
         if (s0 + 16 * kTB > L) {
-  #pragma unroll
+#pragma unroll
           for (int rg = 0; rg < NG; ++rg)
-  #pragma unroll
+#pragma unroll
             for (int tb = 0; tb < kTB; ++tb)
-  #pragma unroll
+#pragma unroll
               for (int r = 0; r < 4; ++r) {
                 const int tok = s0 + tb * 16 + 4 * g + r;
                 sacc[rg][tb][r] += mask_bias(tok, L, end, n_of[rg], s_anc);
@@ -1224,10 +1224,10 @@ void tree_attn_rg(Args a) {
         // lazy rescale of any group whose maximum grew.
         float m_tile[NG];
         bool grow_any = false;
-  #pragma unroll
+#pragma unroll
         for (int rg = 0; rg < NG; ++rg) {
           float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
-  #pragma unroll
+#pragma unroll
           for (int i = 3; i + 1 < 4 * kTB; i += 2)
             mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
           mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
@@ -1236,12 +1236,12 @@ void tree_attn_rg(Args a) {
           grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
         }
         if (__builtin_expect(__ballot(grow_any) != 0, 0)) {
-  #pragma unroll
+#pragma unroll
           for (int rg = 0; rg < NG; ++rg) {
             if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
               const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
               l_run[rg] *= alpha;
-  #pragma unroll
+#pragma unroll
               for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
               m_run[rg] = m_tile[rg];
             }
@@ -1250,24 +1250,24 @@ void tree_attn_rg(Args a) {
         // V^T fragment i: k-step hs * kPV + i / kDBlk, column block i % kDBlk.
         Pack8 vf[kVFrags];
         auto load_v = [&](Pack8& f, int i) {
-  #pragma unroll
+#pragma unroll
           for (int h = 0; h < 2; ++h) {
             const int rows0 = 32 * (hs * kPV + i / kDBlk) + 16 * h;   // multiple of 8: swizzle-free
             f.h[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                 (lds_i16x4*)(vt + rows0 * G::kRowBytes + v_off[i % kDBlk]));
           }
         };
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
         bf16x8 pb[NG][kPV];
-  #pragma unroll
+#pragma unroll
         for (int rg = 0; rg < NG; ++rg) {
           const float nm = m_run[rg] == -INFINITY ? 0.f : -m_run[rg];
           float l0 = 0.f, l1 = 0.f;
-  #pragma unroll
+#pragma unroll
           for (int kt2 = 0; kt2 < kPV; ++kt2) {
             bf16x8 v8;
-  #pragma unroll
+#pragma unroll
             for (int j = 0; j < 8; ++j)
               v8[j] = (__bf16)fast_exp2(fmaf(sacc[rg][2 * kt2 + (j >> 2)][j & 3], cs, nm));
             pb[rg][kt2] = v8;
@@ -1278,10 +1278,10 @@ void tree_attn_rg(Args a) {
           }
           l_run[rg] += l0 + l1;
         }
-  #pragma unroll
+#pragma unroll
         for (int i = 0; i < kVFrags; ++i) {
           if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
-  #pragma unroll
+#pragma unroll
           for (int rg = 0; rg < NG; ++rg)
             oacc[rg][i % kDBlk] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 vf[i].v, pb[rg][i / kDBlk], oacc[rg][i % kDBlk], 0, 0, 0);
