@@ -1015,8 +1015,8 @@ void tree_attn_rg(Args a) {
   constexpr int kPV = 2 / HT;
   constexpr int kKFrags = kTB * kKSteps;           // K operand fragments per step
   constexpr int kVFrags = kPV * kDBlk;             // V^T operand fragments per step
-  constexpr int kAheadK = 3;                       // K reads in flight ahead of their MFMAs
-  constexpr int kAheadV = 3;                       // V^T reads in flight ahead of their MFMAs
+  constexpr int kAheadK = 4;                       // K reads in flight ahead of their MFMAs
+  constexpr int kAheadV = 4;                       // V^T reads in flight ahead of their MFMAs
   // Each iteration waits until its tile has landed while the NBUF - 2 tiles
   // issued after it may still be in flight (2 instructions per block).
   constexpr int kVmWait = waitcnt_vm((NBUF - 2) * 2 * kDmaBlocks);
