@@ -144,15 +144,6 @@ CURE_DEV Top2 top2_stage(const Top2& t) {
   return top2_merge(t, o);
 }
 
-CURE_DEV Top2 top2_wave_reduce(Top2 t) {
-  t = top2_stage<1>(t);
-  t = top2_stage<2>(t);
-  t = top2_stage<4>(t);
-  t = top2_stage<8>(t);
-  t = top2_stage<16>(t);
-  return top2_stage<32>(t);
-}
-
 // Log-sum-exp state: the sum of exp(x - ref) over the entries seen, with a
 // finite reference (a very negative sentinel until the first finite entry).
 constexpr float kLseEmptyRef = -1.0e30f;

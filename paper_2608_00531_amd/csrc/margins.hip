@@ -143,6 +143,46 @@ CURE_DEV float max8(const float (&f)[kVec]) {
   return max3(max3(f[0], f[1], f[2]), max3(f[3], f[4], f[5]), max3(f[6], f[7], f[7]));
 }
 
+// Wave-wide maximum (float) and minimum (int), every lane getting the result:
+// DPP stages 1-8, then the 16- and 32-lane swaps, all on the VALU.
+CURE_DEV float wave_max_raw(float x) {
+  x = max_raw(x, partner<1>(x));
+  x = max_raw(x, partner<2>(x));
+  x = max_raw(x, partner<4>(x));
+  x = max_raw(x, partner<8>(x));
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = max_raw(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max_raw(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+CURE_DEV int wave_min_int(int x) {
+  x = min(x, partner<1>(x));
+  x = min(x, partner<2>(x));
+  x = min(x, partner<4>(x));
+  x = min(x, partner<8>(x));
+  const auto r = __builtin_amdgcn_permlane16_swap((unsigned)x, (unsigned)x, false, false);
+  x = min((int)r[0], (int)r[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
+  return min((int)q[0], (int)q[1]);
+}
+
+// The wave's top 2 (value descending, index ascending) when each lane's own
+// pair is ordered -- (v1, i1) beats (v2, i2) -- and real indices are unique
+// across lanes: first the best of the lanes' first entries, then the best of
+// the other lanes' first entries and the winner's second. Four scalar
+// reductions instead of a butterfly of whole records. With no real entry
+// anywhere every lane is a "winner" and both results are the empty slot.
+CURE_DEV Top2 top2_wave_ordered(const Top2& t) {
+  const float m1 = wave_max_raw(t.v1);
+  const int i1 = wave_min_int(t.v1 == m1 ? t.i1 : INT32_MAX);
+  const bool win = t.v1 == m1 && t.i1 == i1;
+  const float cv = win ? t.v2 : t.v1;
+  const int ci = win ? t.i2 : t.i1;
+  const float m2 = wave_max_raw(cv);
+  const int i2 = wave_min_int(cv == m2 ? ci : INT32_MAX);
+  return {m1, m2, i1, i2};
+}
+
 template <typename T>
 CURE_DEV float load1(const T* p);
 template <>
@@ -324,30 +364,34 @@ __global__ __launch_bounds__(kThreads) void margins_kernel(Args a) {
   // The wave's top-2 entries lie in its two best vectors (by maximum
   // descending, position ascending) together with the lanes' scalar-tail
   // entries. The lanes' vector records are merged first (positions as indices;
-  // "none" is (-inf, INT32_MAX), which every real vector beats) and only those
-  // two vectors are reloaded, by lanes 0 and 1: two 16-byte reads per wave
-  // instead of one scattered read per lane. The log-sum-exp reduction runs
-  // while they are in flight.
+  // "none" is (-inf, INT32_MAX), which every real vector beats); then lanes
+  // 0-7 reread the entries of the best vector and lanes 8-15 those of the
+  // second, one entry per lane, so that each lane adds a single entry to its
+  // own top 2. The log-sum-exp reduction runs while the reads are in flight.
+  // Every lane's top 2 is ordered and its indices are its own, so the wave
+  // reductions take the ordered form.
   const int lane = tid & (kWave - 1);
-  int mine = INT32_MAX;
-  Raw8<T> k;
+  int mine = INT32_MAX;                          // entry index within the chunk
+  uint32_t raw = 0;
   if (kVecPath) {
-    const Top2 bv = top2_wave_reduce(Top2{bm1, bm2, bv1 < 0 ? INT32_MAX : bv1,
-                                          bv2 < 0 ? INT32_MAX : bv2});
-    mine = lane == 0 ? bv.i1 : (lane == 1 ? bv.i2 : INT32_MAX);
-    if (mine != INT32_MAX)
-      k.load(chunk_rsrc(x + begin, (uint32_t)nvec * Raw8<T>::kBytes), (uint32_t)mine * Raw8<T>::kBytes);
+    const Top2 bv = top2_wave_ordered(Top2{bm1, bm2, bv1 < 0 ? INT32_MAX : bv1,
+                                           bv2 < 0 ? INT32_MAX : bv2});
+    const int pick = lane < kVec ? bv.i1 : (lane < 2 * kVec ? bv.i2 : INT32_MAX);
+    if (pick != INT32_MAX) {
+      mine = pick * kVec + (lane & (kVec - 1));
+      const __amdgpu_buffer_rsrc_t r1 = chunk_rsrc(x + begin, (uint32_t)nvec * Raw8<T>::kBytes);
+      if (sizeof(T) == 2)
+        raw = __builtin_amdgcn_raw_buffer_load_b16(r1, mine * 2, 0, kNonTemporal);
+      else
+        raw = __builtin_amdgcn_raw_buffer_load_b32(r1, mine * 4, 0, kNonTemporal);
+    }
   }
   Lse s = lse_wave_reduce(Lse{ref, sum});
-  if (kVecPath && mine != INT32_MAX) {
-    float f[kVec];
-    k.widen(f);
-#pragma unroll
-    for (int j = 0; j < kVec; ++j) top2_push(t, f[j], begin + mine * kVec + j);
-  }
+  if (kVecPath && mine != INT32_MAX)
+    top2_push(t, sizeof(T) == 2 ? bf16_to_f32((uint16_t)raw) : __uint_as_float(raw), begin + mine);
 
   // Workgroup reduction.
-  t = top2_wave_reduce(t);
+  t = top2_wave_ordered(t);
   const int wave = tid / kWave;
   if ((tid & (kWave - 1)) == 0) { s_top[wave] = t; s_lse[wave] = s; }
   __syncthreads();
