@@ -100,6 +100,53 @@ def test_ties_across_chunks_go_to_lowest_index(dtype):
     assert got["top2_idx"][0].tolist() == [70000, 127999, 40000, 77777]
 
 
+def _placement_rows(vocab, rng):
+    """Eight rows whose top entries sit where the kernel's wave-wide merges of
+    the lanes' best vectors must get them right. Entry 8 v + j is entry j of
+    16-byte vector v; with the row in one chunk, vectors v, v + 256 and v + 512
+    belong to the same lane, vectors 0-63 to wave 0 and 64-127 to wave 1."""
+    E = lambda v, j: 8 * v + j
+    r = rng.uniform(-4.0, 4.0, size=(8, vocab)).astype(np.float32)
+    r[0, [E(5, 3), E(261, 6), E(517, 0)]] = [20.0, 19.0, 18.0]   # one lane's vectors
+    r[1, [E(7, 1), E(7, 6), E(300, 2)]] = [20.0, 19.5, 19.0]     # runner-up in the best vector
+    r[2, [E(300, 2), E(40, 7)]] = 20.0                           # equal maxima in two lanes
+    r[3, [E(200, 1), E(70, 5), E(130, 0)]] = 20.0                # and across waves
+    r[4, [E(9, 0), E(9, 4), E(3, 7)]] = [20.0, 19.0, 19.0]       # runner-up tie across vectors
+    r[5, :] = 1.0                                                # constant row
+    r[6, :] = -np.inf
+    r[6, E(100, 3)] = 0.5                                        # one finite entry
+    r[7, [vocab - 1, vocab - 9]] = [20.0, 19.75]                 # the row's last vectors
+    return r
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("vocab", [65536, 128256])
+@pytest.mark.parametrize("nrows", [8, 520])
+def test_top2_vector_placements(dtype, vocab, nrows):
+    """Top-2 exactness when the two best vectors share a lane, the runner-up is in
+    the best vector, or equal maxima sit in several lanes and waves (the lowest
+    index wins). 520 rows keep each row in one chunk; 8 rows split each row."""
+    say("margins top-2 placements", dtype, vocab, nrows)
+    rng = np.random.default_rng(vocab + nrows)
+    special = _rows(_placement_rows(vocab, rng), dtype)
+    x = np.empty((nrows, vocab), special.dtype)       # bf16: raw bits
+    x[:8] = special
+    if nrows > 8:
+        x[8:] = _rows(rng.uniform(-4.0, 4.0, size=(nrows - 8, vocab)), dtype)
+    got = _run_raw(x[None], dtype)
+    ref = oracle.margins(special, dtype)
+    g = {k: v.reshape(-1)[:8].cpu().numpy() for k, v in got.items() if k in ref}
+    for key in ("top1_idx", "top2_idx", "top1_val", "top2_val"):
+        assert np.array_equal(g[key], ref[key]), key
+    assert np.array_equal(g["margin"], ref["margin_f32"], equal_nan=True)
+    fin = np.isfinite(ref["lse"])
+    assert np.array_equal(np.isfinite(g["lse"]), fin)
+    assert np.all(np.abs(g["lse"][fin] - ref["lse"][fin]) <= MARGIN_TOL)
+    E = lambda v, j: 8 * v + j
+    assert g["top1_idx"].tolist()[:6] == [E(5, 3), E(7, 1), E(40, 7), E(70, 5), E(9, 0), 0]
+    assert g["top2_idx"].tolist()[:6] == [E(261, 6), E(7, 6), E(300, 2), E(130, 0), E(3, 7), 1]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_unaligned_row_stride_uses_scalar_path(dtype):
     say("margins unaligned ld", dtype)
