@@ -5,12 +5,14 @@
 // Work decomposition: each row is cut into `splits` contiguous chunks, one
 // 256-thread workgroup per (row, chunk). A lane reads 16-byte vectors of 8
 // entries and keeps an online log-sum-exp plus its two best vectors ranked by
-// (vector maximum descending, position ascending). A lane's top-2 entries
-// always lie in those two vectors: the top-1 sits in the first vector holding
-// the largest value, and the top-2 is either beside it or is the maximum of the
-// best other vector. So the streaming loop tracks vectors branch-free (their
-// raw bits stay in registers), and only at the end does each lane rank those
-// 16 entries exactly (value descending, index ascending).
+// (vector maximum descending, position ascending). The top-2 entries of any
+// set of vectors always lie in its two best vectors: the top-1 sits in the
+// first vector holding the largest value, and the top-2 is either beside it or
+// is the maximum of the best other vector. So the streaming loop tracks only
+// each lane's two best vectors' maxima and positions, branch-free; at the end
+// the wave merges its lanes' records, rereads the 16 entries of its own two
+// best vectors (one per lane) and ranks them exactly (value descending, index
+// ascending).
 //
 // With one chunk per row the workgroup writes the row's results itself. With
 // several, chunk results go to the workspace and margins_finish (one workgroup
