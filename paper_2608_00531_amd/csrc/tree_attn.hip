@@ -891,24 +891,6 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
 #pragma unroll
         for (int r = 0; r < 4; ++r) sacc[tb][r] += mask_bias(t0 + tb * 16 + 4 * g + r, L, end, n, s_anc);
     }
-    // Row maximum over the lane's 16 scores (eight v_max3), then its 3 partners.
-    float mb = max3_raw(sacc[0][0], sacc[0][1], sacc[0][2]);
-#pragma unroll
-    for (int i = 3; i < 15; i += 2)
-      mb = max3_raw(mb, sacc[i >> 2][i & 3], sacc[(i + 1) >> 2][(i + 1) & 3]);
-    mb = max3_raw(mb, sacc[3][3], sacc[3][3]);
-    mb = max3_raw(mb, partner<16>(mb), mb);
-    const float m_tile = max_halves(mb) * cs;
-    const bool grow = m_tile > m_run + kRescaleLog2;
-    if (__builtin_expect(__ballot(grow) != 0, 0)) {
-      if (grow) {
-        const float alpha = fast_exp2(m_run - m_tile);
-        l_run *= alpha;
-#pragma unroll
-        for (int i = 0; i < kDBlk; ++i) oacc[i] *= alpha;
-        m_run = m_tile;
-      }
-    }
     // V^T fragment i: k-step i / kDBlk, column block i % kDBlk. The first
     // kAheadV go out before the exponentials, which then hide their latency.
     Pack8 vf[kVFrags];
@@ -922,20 +904,57 @@ __global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a
     };
 #pragma unroll
     for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
-    const float nm = m_run == -INFINITY ? 0.f : -m_run;
+    // Probabilities against the running reference m_run, bf16 for the P V
+    // product, and the lane's share of the row sums from the same bf16 values.
     bf16x8 pb[2];                                  // k-steps kt = 0, 1 (blocks 2 kt, 2 kt + 1)
     float l0 = 0.f, l1 = 0.f;
+    auto exps = [&](float nm) {
+      l0 = 0.f;
+      l1 = 0.f;
 #pragma unroll
-    for (int kt2 = 0; kt2 < 2; ++kt2) {
-      bf16x8 v8;
+      for (int kt2 = 0; kt2 < 2; ++kt2) {
+        bf16x8 v8;
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        v8[j] = (__bf16)fast_exp2(fmaf(sacc[2 * kt2 + (j >> 2)][j & 3], cs, nm));
-      pb[kt2] = v8;
-      l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
-      l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
-      l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
-      l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+        for (int j = 0; j < 8; ++j)
+          v8[j] = (__bf16)fast_exp2(fmaf(sacc[2 * kt2 + (j >> 2)][j & 3], cs, nm));
+        pb[kt2] = v8;
+        l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[0], v8[1]}, ones, l0, false);
+        l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[2], v8[3]}, ones, l1, false);
+        l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
+        l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
+      }
+    };
+    // The reference moves lazily, when a row's maximum rises by more than 2^8.
+    // The tile's row maxima are reduced only when that can happen: when a row
+    // has no reference yet, or when some lane's probabilities sum to more than
+    // 2^8 (otherwise none of them exceeds 2^8, so no row's maximum rose that
+    // far). Up to rounding at the threshold the probabilities are those of
+    // reducing the maximum on every tile.
+    bool have = false, check = true;
+    if (__ballot(m_run == -INFINITY) == 0) {
+      exps(-m_run);
+      have = true;
+      check = __ballot(!(l0 + l1 <= 256.f)) != 0;
+    }
+    if (__builtin_expect(check, 0)) {
+      // Row maximum over the lane's 16 scores (eight v_max3), then its 3 partners.
+      float mb = max3_raw(sacc[0][0], sacc[0][1], sacc[0][2]);
+#pragma unroll
+      for (int i = 3; i < 15; i += 2)
+        mb = max3_raw(mb, sacc[i >> 2][i & 3], sacc[(i + 1) >> 2][(i + 1) & 3]);
+      mb = max3_raw(mb, sacc[3][3], sacc[3][3]);
+      mb = max3_raw(mb, partner<16>(mb), mb);
+      const float m_tile = max_halves(mb) * cs;
+      const bool grow = m_tile > m_run + kRescaleLog2;
+      const bool grew = __ballot(grow) != 0;
+      if (grow) {
+        const float alpha = fast_exp2(m_run - m_tile);
+        l_run *= alpha;
+#pragma unroll
+        for (int i = 0; i < kDBlk; ++i) oacc[i] *= alpha;
+        m_run = m_tile;
+      }
+      if (!have || grew) exps(m_run == -INFINITY ? 0.f : -m_run);
     }
     l_run += l0 + l1;
 
@@ -1220,33 +1239,6 @@ void tree_attn_rg(Args a) {
                 sacc[rg][tb][r] += mask_bias(tok, L, end, n_of[rg], s_anc);
               }
         }
-        // Row maxima (the lane's 4 kTB scores, then its 3 partners), then the
-        // lazy rescale of any group whose maximum grew.
-        float m_tile[NG];
-        bool grow_any = false;
-#pragma unroll
-        for (int rg = 0; rg < NG; ++rg) {
-          float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
-#pragma unroll
-          for (int i = 3; i + 1 < 4 * kTB; i += 2)
-            mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
-          mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
-          mb = max3_raw(mb, partner<16>(mb), mb);
-          m_tile[rg] = max_halves(mb) * cs;
-          grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
-        }
-        if (__builtin_expect(__ballot(grow_any) != 0, 0)) {
-#pragma unroll
-          for (int rg = 0; rg < NG; ++rg) {
-            if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
-              const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
-              l_run[rg] *= alpha;
-#pragma unroll
-              for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
-              m_run[rg] = m_tile[rg];
-            }
-          }
-        }
         // V^T fragment i: k-step hs * kPV + i / kDBlk, column block i % kDBlk.
         Pack8 vf[kVFrags];
         auto load_v = [&](Pack8& f, int i) {
@@ -1259,10 +1251,11 @@ void tree_attn_rg(Args a) {
         };
 #pragma unroll
         for (int i = 0; i < kAheadV; ++i) load_v(vf[i], i);
+        // Probabilities of group rg against its running reference, bf16 for
+        // the P V product, and the lane's share of the row sum from them.
         bf16x8 pb[NG][kPV];
-#pragma unroll
-        for (int rg = 0; rg < NG; ++rg) {
-          const float nm = m_run[rg] == -INFINITY ? 0.f : -m_run[rg];
+        float lsum[NG];
+        auto exps = [&](int rg, float nm) {
           float l0 = 0.f, l1 = 0.f;
 #pragma unroll
           for (int kt2 = 0; kt2 < kPV; ++kt2) {
@@ -1276,8 +1269,61 @@ void tree_attn_rg(Args a) {
             l0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[4], v8[5]}, ones, l0, false);
             l1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v8[6], v8[7]}, ones, l1, false);
           }
-          l_run[rg] += l0 + l1;
+          lsum[rg] = l0 + l1;
+        };
+        // The lazy rescale of the 16-row kernel: each group's reference moves
+        // when its row maximum rises by more than 2^8, and the maxima are
+        // reduced only when that can happen (a row without a reference, or a
+        // lane whose probabilities sum to more than 2^8).
+        bool no_ref = false;
+#pragma unroll
+        for (int rg = 0; rg < NG; ++rg) no_ref |= m_run[rg] == -INFINITY;
+        bool have = false, check = true;
+        if (__ballot(no_ref) == 0) {
+          bool big = false;
+#pragma unroll
+          for (int rg = 0; rg < NG; ++rg) {
+            exps(rg, -m_run[rg]);
+            big |= !(lsum[rg] <= 256.f);
+          }
+          have = true;
+          check = __ballot(big) != 0;
         }
+        if (__builtin_expect(check, 0)) {
+          // Row maxima (the lane's 4 kTB scores, then its 3 partners).
+          float m_tile[NG];
+          bool grow_any = false;
+#pragma unroll
+          for (int rg = 0; rg < NG; ++rg) {
+            float mb = max3_raw(sacc[rg][0][0], sacc[rg][0][1], sacc[rg][0][2]);
+#pragma unroll
+            for (int i = 3; i + 1 < 4 * kTB; i += 2)
+              mb = max3_raw(mb, sacc[rg][i >> 2][i & 3], sacc[rg][(i + 1) >> 2][(i + 1) & 3]);
+            mb = max3_raw(mb, sacc[rg][kTB - 1][3], sacc[rg][kTB - 1][3]);
+            mb = max3_raw(mb, partner<16>(mb), mb);
+            m_tile[rg] = max_halves(mb) * cs;
+            grow_any |= m_tile[rg] > m_run[rg] + kRescaleLog2;
+          }
+          const bool grew = __ballot(grow_any) != 0;
+          if (grew) {
+#pragma unroll
+            for (int rg = 0; rg < NG; ++rg) {
+              if (m_tile[rg] > m_run[rg] + kRescaleLog2) {
+                const float alpha = fast_exp2(m_run[rg] - m_tile[rg]);
+                l_run[rg] *= alpha;
+#pragma unroll
+                for (int i = 0; i < kDBlk; ++i) oacc[rg][i] *= alpha;
+                m_run[rg] = m_tile[rg];
+              }
+            }
+          }
+          if (!have || grew) {
+#pragma unroll
+            for (int rg = 0; rg < NG; ++rg) exps(rg, m_run[rg] == -INFINITY ? 0.f : -m_run[rg]);
+          }
+        }
+#pragma unroll
+        for (int rg = 0; rg < NG; ++rg) l_run[rg] += lsum[rg];
 #pragma unroll
         for (int i = 0; i < kVFrags; ++i) {
           if (i + kAheadV < kVFrags) load_v(vf[i + kAheadV], i + kAheadV);
