@@ -14,7 +14,7 @@ import pytest
 import torch
 
 import paper_2608_00531_amd as pc
-from synth import preset, make_workload
+from synth import preset, make_workload, bf16_round
 from parity_util import say, upload, gpu_attn, oracle_attn, check_attn, Timer, LSE_TOL
 
 pytestmark = pytest.mark.gpu
@@ -352,6 +352,50 @@ def test_nonpositive_scale_takes_the_general_path():
     dev = upload(w)
     o, lse, st = gpu_attn(w, dev)
     torch.cuda.synchronize()
+    ref_o, ref_l = oracle_attn(w)
+    check_attn(w, o, lse, ref_o, ref_l)
+
+
+def _climbing_keys(w):
+    """Keys whose scores climb along each sequence (a gain from 1 to 7) and two
+    late context tokens 60 times stronger still: the running softmax
+    reference has to move several times inside one split, and against the
+    reference before them the spikes' probabilities (scores near 2^150 times
+    the earlier maximum for some rows) overflow float32."""
+    bf16 = w.dtype == "bf16"
+    k = (w.k.astype(np.uint32) << np.uint32(16)).view(np.float32) if bf16 else w.k.copy()
+    for b in range(w.batch):
+        off, L = int(w.kv_off[b]), int(w.ctx_len[b]) + int(w.n_nodes[b])
+        k[off:off + L] *= (1.0 + 6.0 * np.arange(L) / max(L - 1, 1)).astype(np.float32)[:, None, None]
+        for frac in (0.55, 0.9):
+            tok = int(frac * (int(w.ctx_len[b]) - 1))
+            k[off + tok] *= np.float32(60.0)
+    w.k = bf16_round(k) if bf16 else k
+
+
+@pytest.mark.parametrize("case", ["rows128", "rows192", "rows320", "valu_bf16"])
+@pytest.mark.parametrize("kv_split", [0, 1])
+def test_softmax_reference_moves_and_spikes(case, kv_split):
+    """The tiles' probabilities are taken against a running reference that
+    moves only when a row's maximum rises by more than 2^8; the kernels check
+    for that after the exponentials and redo a tile when it happens. Climbing
+    scores and late spikes make it happen often, including probabilities that
+    overflow before the redo, on the 16-row kernel (128 and 192 rows), the
+    three-row-group kernel (320 rows) and the bf16 vector-ALU path, with the
+    planned splits and with one split per sequence. (fp32 inputs of these
+    magnitudes are left out: their scores, near 1e4 before scaling, carry
+    fp32 rounding of a few 1e-4 themselves, beyond the absolute fp32 bars.)"""
+    say("attn climbing scores", case, "kv_split", kv_split)
+    n_ufp = {"rows192": 8, "rows320": 16}.get(case, 4)
+    w = make_workload("c", batch=2,
+                      ctx_lens=[1500, 3000], chain_len=16, n_ufp=n_ufp, branch_depth=4,
+                      seed=71)
+    _climbing_keys(w)
+    dev = upload(w)
+    flags = pc.CURE_ATTN_FORCE_VALU if case == "valu_bf16" else 0
+    o, lse, st = gpu_attn(w, dev, kv_split=kv_split, flags=flags)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK] * w.batch
     ref_o, ref_l = oracle_attn(w)
     check_attn(w, o, lse, ref_o, ref_l)
 
