@@ -701,8 +701,9 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 // ---------------------------------------------------------------------------
 // MFMA split kernel with 16 query rows per wave (v_mfma_f32_16x16x32_bf16).
 //
-// Same tile stream, LDS layout, tree mask and online softmax as the 32-row
-// kernel above, at half the registers per wave, so that two 8-wave
+// Same tile stream, LDS layout, tree mask and lazily rescaled online softmax
+// as the 32-row kernel above (here a tile's row maxima are reduced only when a
+// rescale could be due), at half the registers per wave, so that two 8-wave
 // workgroups (four waves per SIMD) share a CU, and row blocks of up to 256
 // rows fit one 16-wave workgroup with the rows spread evenly over the SIMDs.
 // Wider trees take several row blocks of equal size (a multiple of 16 rows).
