@@ -724,8 +724,10 @@ __global__ __launch_bounds__(64 * NW, NBUF > 2 ? 1 : 2) void tree_attn_mfma(Args
 //   already holds from blocks 2 kt and 2 kt + 1, so P needs no exchange.
 //     A = V^T: two transposed reads of 4 tokens x 16 columns per 16 lanes
 //     D register r = O column 16 db + 4 g + r of row c
+// At most 128 VGPRs (four waves per SIMD): two 8-wave workgroups share a CU
+// whenever a launch has more workgroups than CUs.
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW, NW <= 8 ? 2 : 1) void tree_attn_m16(Args a) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4))) void tree_attn_m16(Args a) {
   using G = TileGeo<D>;
   constexpr int kKSteps = D / 32;                  // k-steps for Q K^T
   constexpr int kDBlk = D / 16;                    // 16-column blocks of O^T
