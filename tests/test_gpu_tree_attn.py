@@ -325,6 +325,27 @@ def test_long_context_full_size_sampled():
     check_attn(w, o, lse, ref_o, ref_l, sample=sample)
 
 
+@pytest.mark.parametrize("kv_split", [0, 2])
+def test_more_workgroups_than_cus_sampled(kv_split):
+    # 64 sequences x 8 kv-heads of 32-node trees (128 rows): 512 workgroups of
+    # the 8-wave 16-row kernel at the planned single split (1024 at two splits,
+    # then merged), more than the CUs, so two of them share a CU.
+    say("attn 64 sequences, more workgroups than CUs, kv_split", kv_split)
+    rng = np.random.default_rng(12)
+    ctx = [int(x) for x in rng.integers(1, 1600, 64)]
+    w = make_workload("wide", batch=64, ctx_lens=ctx, chain_len=16, n_ufp=4, branch_depth=4,
+                      seed=13)
+    dev = upload(w)
+    o, lse, st = gpu_attn(w, dev, kv_split=kv_split)
+    torch.cuda.synchronize()
+    assert st.tolist() == [pc.CURE_OK] * w.batch
+    sample = [(b, int(n)) for b in range(w.batch) for n in rng.choice(32, 2, replace=False)]
+    sample += [(0, 0), (63, 31)]
+    with Timer("oracle"):
+        ref_o, ref_l = oracle_attn(w, sample=sample)
+    check_attn(w, o, lse, ref_o, ref_l, sample=sample)
+
+
 def test_largest_sweep_tree_full_size_sampled():
     # Batch 8, context 8192, 80 nodes: 320 rows per kv-head, one block of seven
     # 48-row waves, in the launch configuration the budget sweep times.
