@@ -1387,10 +1387,14 @@ void tree_attn_rg(Args a) {
 // instruction covers 64/(D/4) splits (2 at D=128, 4 at D=64). A batch of NB
 // such loads, with each split's LSE alongside, is issued before anything is
 // reduced, and NB is the smallest of 2, 4, 8 that covers the launch's largest
-// split count when it can: the whole merge is then one memory round trip,
-// with no more registers held than that needs. The lane groups holding
-// different splits are combined with xor shuffles at the end.
-template <int D, int NB>
+// split count when it can: the partials then take one memory round trip,
+// with no more registers held than that needs. When every sequence has the
+// launch's largest split count that batch goes out with the loads of the
+// sequence's sizes; otherwise (kOwnSplits, a ragged batch) the sizes come
+// first and each row reads only its own splits' slots, instead of fetching
+// slots it would discard. The lane groups holding different splits are
+// combined with xor shuffles at the end.
+template <int D, int NB, bool kOwnSplits>
 __global__ __launch_bounds__(256) void attn_merge(Args a) {
   constexpr int kLanesPerSplit = D / 4;
   constexpr int kSplitsPerLoad = kWave / kLanesPerSplit;
@@ -1421,18 +1425,24 @@ __global__ __launch_bounds__(256) void attn_merge(Args a) {
       l[u] = ok ? a.part_lse[p0 + sp] : -INFINITY;
     }
   };
-  load_batch(0, a.max_splits);
+  if (!kOwnSplits) load_batch(0, a.max_splits);
   const int n_raw = a.n_nodes[b];
   const int L = a.ctx_len[b];
   const int N = min(n_raw, a.n_max);
   if (n >= N) return;
   const int S = split_count(L + N, N, a.tps, a.max_splits);
   if (S <= 1) return;
+  if (kOwnSplits) {
+    load_batch(0, S);
+  } else {
+    // Slots past this sequence's own split count get zero weight (the plan
+    // comes from host copies of the sizes, so this cannot be taken for granted).
 #pragma unroll
-  for (int u = 0; u < NB; ++u) {
-    if (u * kSplitsPerLoad + sub >= S) {
-      v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-      l[u] = -INFINITY;
+    for (int u = 0; u < NB; ++u) {
+      if (u * kSplitsPerLoad + sub >= S) {
+        v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        l[u] = -INFINITY;
+      }
     }
   }
   // Reference maximum: from the loaded batch when it holds every split, else
@@ -1505,6 +1515,7 @@ struct Plan {
   int row_blocks;
   int tps;
   int max_splits;
+  bool uniform_splits;  // every sequence with nodes has max_splits splits (host sizes)
 };
 
 // The three-row-group kernel as instantiated: 8 waves of up to 48 query rows
@@ -1635,6 +1646,13 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t n_max,
   tps = std::max<int64_t>(tps, round_tile((t_max + kMaxGridY - 1) / kMaxGridY));
   p.tps = (int)std::min<int64_t>(tps, INT32_MAX / 2);
   p.max_splits = t_max > 0 ? (int)((t_max + p.tps - 1) / p.tps) : 0;
+  p.uniform_splits = true;
+  for (int b = 0; b < batch; ++b) {
+    const int N = std::min(host_n_nodes[b], n_max);
+    if (N <= 0) continue;
+    const int64_t T = (int64_t)host_ctx_len[b] + N;
+    if ((T + p.tps - 1) / p.tps < p.max_splits) p.uniform_splits = false;
+  }
   return p;
 }
 
@@ -1788,15 +1806,22 @@ extern "C" cure_status cure_tree_attn(const void* q, const void* k, const void* 
     const dim3 mgrid((unsigned)((hq + 3) / 4), (unsigned)n_max, (unsigned)batch);
     const int per_load = 256 / d;                       // splits per merge load
     const int nb = p.max_splits <= 2 * per_load ? 2 : p.max_splits <= 4 * per_load ? 4 : 8;
+    const bool own = !p.uniform_splits;
+#define CURE_MERGE(DD, NN)                                                                   \
+    do {                                                                                     \
+      if (own) hipLaunchKernelGGL((attn_merge<DD, NN, true>), mgrid, dim3(256), 0, st, a);   \
+      else hipLaunchKernelGGL((attn_merge<DD, NN, false>), mgrid, dim3(256), 0, st, a);      \
+    } while (0)
     if (d == 128) {
-      if (nb == 2) hipLaunchKernelGGL((attn_merge<128, 2>), mgrid, dim3(256), 0, st, a);
-      else if (nb == 4) hipLaunchKernelGGL((attn_merge<128, 4>), mgrid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((attn_merge<128, 8>), mgrid, dim3(256), 0, st, a);
+      if (nb == 2) CURE_MERGE(128, 2);
+      else if (nb == 4) CURE_MERGE(128, 4);
+      else CURE_MERGE(128, 8);
     } else {
-      if (nb == 2) hipLaunchKernelGGL((attn_merge<64, 2>), mgrid, dim3(256), 0, st, a);
-      else if (nb == 4) hipLaunchKernelGGL((attn_merge<64, 4>), mgrid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((attn_merge<64, 8>), mgrid, dim3(256), 0, st, a);
+      if (nb == 2) CURE_MERGE(64, 2);
+      else if (nb == 4) CURE_MERGE(64, 4);
+      else CURE_MERGE(64, 8);
     }
+#undef CURE_MERGE
   }
   return launch_status();
 }
